@@ -1,0 +1,319 @@
+// Host plan builder: validation, the kept-token slot table with span-preserving
+// positions (Section 3.2 "Output and Reuse"), per-segment and per-suffix-token
+// RoPE cos/sin tables computed in float64, the page assignment and the
+// attention work list.  Pure host code: no HIP call happens here, so plans can
+// be built and inspected on a machine without a GPU.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <limits>
+#include <sstream>
+
+#include "plan.hpp"
+
+namespace c2kv {
+namespace {
+
+constexpr int64_t kI32Max = std::numeric_limits<int32_t>::max();
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int32_t ceil_div(int64_t a, int64_t b) { return static_cast<int32_t>((a + b - 1) / b); }
+
+template <typename... Args>
+std::string fmt(Args&&... args) {
+  std::ostringstream os;
+  (os << ... << args);
+  return os.str();
+}
+
+// theta_i = base^(-2i/D), i < D/2, in float64 (RoPE frequencies).
+std::vector<double> rope_theta(int D, double base) {
+  std::vector<double> th(D / 2);
+  for (int i = 0; i < D / 2; ++i) th[i] = std::pow(base, -2.0 * i / D);
+  return th;
+}
+
+}  // namespace
+
+c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
+                       int32_t suffix_len, const c2kv_plan_opts* opts, Plan& p,
+                       std::string& err) {
+  // ---- attention shape ----------------------------------------------------
+  if (cfg.n_q_heads < 1 || cfg.n_kv_heads < 1 || cfg.n_q_heads % cfg.n_kv_heads != 0) {
+    err = fmt("n_q_heads (", cfg.n_q_heads, ") must be a positive multiple of n_kv_heads (",
+              cfg.n_kv_heads, ")");
+    return C2KV_E_INVAL;
+  }
+  if (cfg.head_dim <= 0 || cfg.head_dim % 2 != 0) {
+    err = fmt("head_dim must be positive and even, got ", cfg.head_dim);
+    return C2KV_E_INVAL;
+  }
+  if (cfg.head_dim != 64 && cfg.head_dim != 128) {
+    err = fmt("head_dim ", cfg.head_dim, " not built (64 or 128)");
+    return C2KV_E_UNSUPPORTED;
+  }
+  if (cfg.act_dtype != C2KV_F32 && cfg.act_dtype != C2KV_BF16) {
+    err = "act_dtype must be C2KV_F32 or C2KV_BF16";
+    return C2KV_E_INVAL;
+  }
+  if (!(cfg.rope_base > 0.0) || !std::isfinite(cfg.rope_base)) {
+    err = "rope_base must be positive and finite";
+    return C2KV_E_INVAL;
+  }
+  if (!std::isfinite(cfg.softmax_scale)) {
+    err = "softmax_scale must be finite";
+    return C2KV_E_INVAL;
+  }
+  if (suffix_len < 1) {
+    err = fmt("suffix_len must be >= 1, got ", suffix_len);
+    return C2KV_E_INVAL;
+  }
+
+  // ---- options --------------------------------------------------------------
+  c2kv_plan_opts o{};
+  if (opts) o = *opts;
+  if (o.page_size == 0) o.page_size = 64;
+  if (o.page_size < 0 || o.page_size % kKeyTile != 0) {
+    err = fmt("page_size must be a positive multiple of ", kKeyTile, ", got ", o.page_size);
+    return C2KV_E_INVAL;
+  }
+  if (o.rows_per_block != 0 && o.rows_per_block != 32 && o.rows_per_block != 64 &&
+      o.rows_per_block != 128 && o.rows_per_block != 256) {
+    err = fmt("rows_per_block must be 0, 32, 64, 128 or 256, got ", o.rows_per_block);
+    return C2KV_E_INVAL;
+  }
+  if (o.kv_splits < 0 || o.num_cus < 0) {
+    err = "kv_splits and num_cus must be >= 0";
+    return C2KV_E_INVAL;
+  }
+  if (o.num_cus == 0) o.num_cus = 256;
+
+  // ---- descriptor -----------------------------------------------------------
+  const int32_t B = d.batch;
+  if (B < 1) { err = fmt("batch must be >= 1, got ", B); return C2KV_E_INVAL; }
+  if (d.n_segments < 0) { err = "n_segments must be >= 0"; return C2KV_E_INVAL; }
+  if (!d.req_seg_off) { err = "req_seg_off is NULL"; return C2KV_E_INVAL; }
+  if (d.req_seg_off[0] != 0 || d.req_seg_off[B] != d.n_segments) {
+    err = "req_seg_off must start at 0 and end at n_segments";
+    return C2KV_E_INVAL;
+  }
+  for (int b = 0; b < B; ++b)
+    if (d.req_seg_off[b + 1] < d.req_seg_off[b]) {
+      err = fmt("req_seg_off decreases at request ", b);
+      return C2KV_E_INVAL;
+    }
+  const int32_t nseg = d.n_segments;
+  if (nseg > 0 && (!d.seg_row0 || !d.seg_span || !d.seg_orig_pos0 || !d.seg_kept_off)) {
+    err = "segment arrays must not be NULL";
+    return C2KV_E_INVAL;
+  }
+  if (nseg > 0 && d.seg_kept_off[0] != 0) { err = "seg_kept_off[0] must be 0"; return C2KV_E_INVAL; }
+  for (int c = 0; c < nseg; ++c) {
+    if (d.seg_kept_off[c + 1] < d.seg_kept_off[c]) {
+      err = fmt("seg_kept_off decreases at segment ", c);
+      return C2KV_E_INVAL;
+    }
+  }
+  const int64_t total_kept = nseg > 0 ? d.seg_kept_off[nseg] : 0;
+  if (total_kept > 0 && !d.kept_idx) { err = "kept_idx is NULL"; return C2KV_E_INVAL; }
+  if (total_kept > kI32Max) { err = "too many kept tokens"; return C2KV_E_UNSUPPORTED; }
+
+  p = Plan{};
+  p.cfg = cfg;
+  p.batch = B;
+  p.suffix_len = suffix_len;
+  p.page_size = o.page_size;
+  p.n_segments = nseg;
+  p.group = cfg.n_q_heads / cfg.n_kv_heads;
+  p.softmax_scale = cfg.softmax_scale > 0.f ? cfg.softmax_scale
+                                            : static_cast<float>(1.0 / std::sqrt(double(cfg.head_dim)));
+  p.qscale_log2 = static_cast<float>(double(p.softmax_scale) * 1.4426950408889634);
+
+  // ---- slot table: segments in request order, kept indices ascending --------
+  p.req_slot0.assign(B + 1, 0);
+  p.span_end.assign(B, 0);
+  p.seg_delta.assign(nseg, 0);
+  p.slot_src.reserve(total_kept);
+  p.slot_seg.reserve(total_kept);
+  p.slot_pos.reserve(total_kept);
+  p.slot_delta.reserve(total_kept);
+  for (int b = 0; b < B; ++b) {
+    int64_t cursor = 0, end = 0;
+    for (int c = d.req_seg_off[b]; c < d.req_seg_off[b + 1]; ++c) {
+      const int64_t span = d.seg_span[c];
+      const int64_t row0 = d.seg_row0[c];
+      const int64_t orig0 = d.seg_orig_pos0[c];
+      const int64_t new0 = d.seg_new_pos0 ? int64_t(d.seg_new_pos0[c]) : cursor;
+      if (span < 0) { err = fmt("seg_span[", c, "] < 0"); return C2KV_E_INVAL; }
+      if (row0 < 0) { err = fmt("seg_row0[", c, "] < 0"); return C2KV_E_INVAL; }
+      if (orig0 < 0 || new0 < 0) { err = fmt("negative position at segment ", c); return C2KV_E_INVAL; }
+      const int64_t delta = new0 - orig0;
+      if (new0 + span > kI32Max || orig0 + span > kI32Max || delta > kI32Max || delta < -kI32Max) {
+        err = fmt("positions of segment ", c, " overflow int32");
+        return C2KV_E_INVAL;
+      }
+      p.seg_delta[c] = static_cast<int32_t>(delta);
+      int64_t prev = -1;
+      for (int k = d.seg_kept_off[c]; k < d.seg_kept_off[c + 1]; ++k) {
+        const int64_t j = d.kept_idx[k];
+        if (j < 0 || j >= span) {
+          err = fmt("kept index ", j, " of segment ", c, " outside [0, ", span, ")");
+          return C2KV_E_INVAL;
+        }
+        if (j <= prev) {
+          err = fmt("kept indices of segment ", c, " are not strictly ascending");
+          return C2KV_E_INVAL;
+        }
+        prev = j;
+        const int64_t src = row0 + j;
+        if (src > kI32Max) { err = "pool row beyond int32 range"; return C2KV_E_UNSUPPORTED; }
+        p.slot_src.push_back(static_cast<int32_t>(src));
+        p.slot_seg.push_back(c);
+        p.slot_pos.push_back(static_cast<int32_t>(new0 + j));
+        p.slot_delta.push_back(static_cast<int32_t>(delta));
+        p.max_src_row = std::max<int64_t>(p.max_src_row, src);
+      }
+      cursor = new0 + span;               // span-preserving: advance by n, not m
+      end = std::max(end, new0 + span);
+    }
+    if (end + suffix_len - 1 > kI32Max) {
+      err = fmt("suffix positions of request ", b, " overflow int32");
+      return C2KV_E_INVAL;
+    }
+    p.span_end[b] = static_cast<int32_t>(end);
+    p.req_slot0[b + 1] = static_cast<int32_t>(p.slot_src.size());
+  }
+
+  // ---- pages: each request gets ceil(N_b / page) consecutive pages ----------
+  const int PS = p.page_size;
+  int64_t pages = 0;
+  int32_t maxp = 1;
+  for (int b = 0; b < B; ++b) {
+    const int64_t n = p.req_slot0[b + 1] - p.req_slot0[b];
+    maxp = std::max(maxp, ceil_div(n, PS));
+  }
+  p.max_pages = maxp;
+  p.block_table.assign(size_t(B) * maxp, -1);
+  for (int b = 0; b < B; ++b) {
+    const int64_t n = p.req_slot0[b + 1] - p.req_slot0[b];
+    const int32_t np = ceil_div(n, PS);
+    for (int i = 0; i < np; ++i) p.block_table[size_t(b) * maxp + i] = static_cast<int32_t>(pages + i);
+    pages += np;
+  }
+  if (pages > kI32Max) { err = "too many pages"; return C2KV_E_UNSUPPORTED; }
+  p.n_pages = static_cast<int32_t>(pages);
+  for (int b = 0; b < B; ++b) {
+    const int64_t n = p.req_slot0[b + 1] - p.req_slot0[b];
+    for (int t = 0; t < ceil_div(n, kKeyTile); ++t) {
+      p.compose_tiles.push_back(b);
+      p.compose_tiles.push_back(t);
+    }
+  }
+
+  // ---- attention work list ---------------------------------------------------
+  const int64_t G = p.group, S = suffix_len;
+  const int64_t R = G * S;            // query rows per (request, kv-head)
+  int RB = o.rows_per_block;
+  if (RB == 0) {
+    RB = 32;
+    while (RB < R && RB < 256) RB *= 2;
+  }
+  p.rows_per_block = RB;
+  const int wgs_per_cu = RB >= 256 ? 1 : (RB == 128 ? 2 : 4);
+  const int64_t target = int64_t(o.num_cus) * wgs_per_cu;
+  const int32_t n_rb = ceil_div(R, RB);
+  struct Group { int32_t b, g, row0, nrows, tiles; };
+  std::vector<Group> groups;
+  int64_t total_tiles = 0;
+  for (int b = 0; b < B; ++b) {
+    const int64_t n = p.req_slot0[b + 1] - p.req_slot0[b];
+    const int32_t nct = ceil_div(n, kKeyTile);
+    for (int g = 0; g < cfg.n_kv_heads; ++g)
+      for (int rb = 0; rb < n_rb; ++rb) {
+        const int32_t row0 = rb * RB;
+        const int32_t nrows = static_cast<int32_t>(std::min<int64_t>(RB, R - row0));
+        const int64_t tmax = (row0 + nrows - 1) / G;       // last suffix token in block
+        const int32_t nst = ceil_div(tmax + 1, kKeyTile);
+        groups.push_back({b, g, row0, nrows, nct + nst});
+        total_tiles += nct + nst;
+      }
+  }
+  const int64_t per_item = std::max<int64_t>(2, (total_tiles + target - 1) / target);
+  for (const Group& gr : groups) {
+    int32_t ns = o.kv_splits > 0 ? o.kv_splits : ceil_div(gr.tiles, per_item);
+    ns = std::max(1, std::min(ns, gr.tiles));
+    p.max_splits = std::max(p.max_splits, ns);
+    int32_t part0 = -1;
+    if (ns > 1) {
+      part0 = p.n_partials;
+      p.merges.push_back({gr.b, gr.g, gr.row0, gr.nrows, part0, ns, 0, 0});
+      p.n_partials += ns;
+    }
+    for (int s = 0; s < ns; ++s) {
+      const int32_t t0 = static_cast<int32_t>(int64_t(gr.tiles) * s / ns);
+      const int32_t t1 = static_cast<int32_t>(int64_t(gr.tiles) * (s + 1) / ns);
+      p.items.push_back({gr.b, gr.g, gr.row0, gr.nrows, t0, t1, ns > 1 ? part0 + s : -1, 0});
+    }
+  }
+  // heaviest items first, so the ragged tail of the grid is short
+  std::stable_sort(p.items.begin(), p.items.end(), [](const WorkItem& a, const WorkItem& b) {
+    return (a.tile1 - a.tile0) > (b.tile1 - b.tile0);
+  });
+
+  // ---- workspace image --------------------------------------------------------
+  const int D = cfg.head_dim, H = D / 2;
+  const int64_t total = static_cast<int64_t>(p.slot_src.size());
+  WorkspaceLayout& w = p.ws;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t at = off; off = align256(off + std::max<size_t>(bytes, 4)); return at; };
+  w.req_slot0 = take(sizeof(int32_t) * (B + 1));
+  w.slot_src = take(sizeof(int32_t) * total);
+  w.slot_seg = take(sizeof(int32_t) * total);
+  w.slot_pos = take(sizeof(int32_t) * total);
+  w.seg_cs = take(sizeof(float) * 2 * size_t(std::max(nseg, 1)) * H);
+  w.suf_cs = take(sizeof(float) * 2 * size_t(B) * S * H);
+  w.block_table = take(sizeof(int32_t) * p.block_table.size());
+  w.compose_tiles = take(sizeof(int32_t) * p.compose_tiles.size());
+  w.items = take(sizeof(WorkItem) * p.items.size());
+  w.merges = take(sizeof(MergeGroup) * p.merges.size());
+  w.table_bytes = off;
+  w.part_o = take(sizeof(float) * size_t(p.n_partials) * RB * D);
+  w.part_lse = take(sizeof(float) * size_t(p.n_partials) * RB);
+  w.total = off;
+
+  p.image.assign(w.table_bytes, 0);
+  auto put = [&](size_t at, const void* src, size_t bytes) {
+    if (bytes) std::memcpy(p.image.data() + at, src, bytes);
+  };
+  put(w.req_slot0, p.req_slot0.data(), sizeof(int32_t) * (B + 1));
+  put(w.slot_src, p.slot_src.data(), sizeof(int32_t) * total);
+  put(w.slot_seg, p.slot_seg.data(), sizeof(int32_t) * total);
+  put(w.slot_pos, p.slot_pos.data(), sizeof(int32_t) * total);
+  put(w.block_table, p.block_table.data(), sizeof(int32_t) * p.block_table.size());
+  put(w.compose_tiles, p.compose_tiles.data(), sizeof(int32_t) * p.compose_tiles.size());
+  put(w.items, p.items.data(), sizeof(WorkItem) * p.items.size());
+  put(w.merges, p.merges.data(), sizeof(MergeGroup) * p.merges.size());
+
+  // cos/sin tables: angles in float64, rounded once to float32
+  const std::vector<double> theta = rope_theta(D, cfg.rope_base);
+  float* seg_cs = reinterpret_cast<float*>(p.image.data() + w.seg_cs);
+  for (int c = 0; c < nseg; ++c)
+    for (int i = 0; i < H; ++i) {
+      const double ang = double(p.seg_delta[c]) * theta[i];
+      seg_cs[(size_t(c) * H + i) * 2 + 0] = static_cast<float>(std::cos(ang));
+      seg_cs[(size_t(c) * H + i) * 2 + 1] = static_cast<float>(std::sin(ang));
+    }
+  float* suf_cs = reinterpret_cast<float*>(p.image.data() + w.suf_cs);
+  for (int b = 0; b < B; ++b)
+    for (int64_t t = 0; t < S; ++t)
+      for (int i = 0; i < H; ++i) {
+        const double ang = double(p.span_end[b] + t) * theta[i];
+        const size_t k = ((size_t(b) * S + t) * H + i) * 2;
+        suf_cs[k + 0] = static_cast<float>(std::cos(ang));
+        suf_cs[k + 1] = static_cast<float>(std::sin(ang));
+      }
+  return C2KV_OK;
+}
+
+}  // namespace c2kv

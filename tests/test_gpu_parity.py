@@ -1,0 +1,214 @@
+"""GPU parity of the HIP path (through the C ABI) with the float64 oracle.
+
+Every workload runs both ways: c2kv_compose_attend (gather/decode/turn fused
+into the attention loads) and c2kv_compose followed by c2kv_attend (paged
+cache).  Tolerances are listed in gpu_common.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_17715_amd as c2kv
+import synth
+from gpu_common import Dev, compare, oracle_ref, run_fused, run_paged, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _both_paths(w, what, rows=None, **opts):
+    ref_out, ref_lse, _ = oracle_ref(w, rows=rows)
+    say(f"{what}: fused compose_attend {opts}")
+    out, lse, plan, dev = run_fused(w, **opts)
+    compare(w, out, lse, ref_out, ref_lse, rows=rows, what=f"{what}/fused")
+    say(f"{what}: compose + attend {opts}")
+    out2, lse2, _, _, _ = run_paged(w, dev=dev, plan=plan)
+    compare(w, out2, lse2, ref_out, ref_lse, rows=rows, what=f"{what}/paged")
+    # the two paths round the same values the same way: identical results
+    assert torch.equal(out, out2), what
+    return plan
+
+
+# ---------------------------------------------------------------------------
+# the five workloads at their full sizes
+# ---------------------------------------------------------------------------
+
+def test_tiny_fp32():
+    _both_paths(synth.config(1), "tiny-fp32")
+
+
+def test_llama3_8b_layer_bf16():
+    _both_paths(synth.config(2), "llama3-8b-layer")
+
+
+def test_ragged_batch_bf16():
+    _both_paths(synth.config(3), "ragged-batch")
+
+
+@pytest.mark.parametrize("layer", [0, 31])
+def test_int8_layer(layer):
+    _both_paths(synth.config(4, layer=layer), f"int8-layer{layer}")
+
+
+def test_long_suffix_sampled_rows():
+    """Full 70B-shaped workload (32768 composed slots, S = 2048) in the launch
+    configuration the benchmark times; the oracle computes sampled suffix rows."""
+    w = synth.config(5)
+    rows = [0, 1, 63, 64, 65, 1000, 1023, 1024, 2046, 2047]
+    _both_paths(w, "70b-long-suffix", rows=rows)
+
+
+# ---------------------------------------------------------------------------
+# compose: layout bit-exact, values, delta = 0 copies
+# ---------------------------------------------------------------------------
+
+def _check_pages(w, plan, res):
+    lay = oracle.compose_layout(w.req_seg_off, w.seg_row0, w.seg_span, w.seg_orig_pos0,
+                                w.seg_kept_off, w.kept_idx, w.seg_new_pos0)
+    # layout outputs written by the kernel: bit-exact
+    src = res["src"].cpu().numpy()
+    pos = res["pos"].cpu().numpy()
+    if len(src):
+        np.testing.assert_array_equal(src, np.concatenate(lay["src_row"]))
+        np.testing.assert_array_equal(pos, np.concatenate(lay["p_new"]))
+    np.testing.assert_array_equal(res["bt"].cpu().numpy(), plan.block_table())
+    # page contents against the oracle's composed cache
+    caches = oracle.compose(lay, w.pool_k, w.pool_v, w.pool_dtype, w.rope_base,
+                            w.pool_k_scale, w.pool_v_scale)
+    kp = c2kv.to_numpy_f64(res["k_pages"])
+    vp = c2kv.to_numpy_f64(res["v_pages"])
+    bt = plan.block_table()
+    ps = plan.info["page_size"]
+    rel = 1e-6 if w.act_dtype == "f32" else 2.0 ** -8
+    for b, (kc, vc) in enumerate(caches):
+        n = kc.shape[0]
+        s = np.arange(n)
+        pages = bt[b][s // ps]
+        kg = kp[pages, :, s % ps, :]                    # [n, H, D]
+        vg = vp[pages, :, :, s % ps]                    # [n, H, D] (pages hold V^T)
+        assert np.all(np.abs(kg - kc) <= rel * np.abs(kc) + 1e-6), b
+        assert np.all(np.abs(vg - vc) <= rel * np.abs(vc) + 1e-6), b
+
+
+@pytest.mark.parametrize("pool_dtype", ["f32", "bf16", "i8"])
+def test_compose_pages(pool_dtype):
+    w = synth.small(pool_dtype=pool_dtype, batch=3, keep=("ratio", 0.05, 0.7))
+    for ps in (64, 128):
+        say(f"compose pages {pool_dtype} page_size={ps}")
+        _, _, plan, _, res = run_paged(w, page_size=ps)
+        _check_pages(w, plan, res)
+
+
+def test_compose_delta0_is_a_bit_exact_copy():
+    """With every segment already at its final position (delta = 0), composing
+    bf16 keys is a copy: cos = 1 and sin = 0 are exact."""
+    w = synth.small(pool_dtype="bf16", batch=2, keep=("ratio", 0.1, 0.9))
+    new0 = []
+    for r in range(w.batch):
+        pos = 0
+        for c in range(w.req_seg_off[r], w.req_seg_off[r + 1]):
+            new0.append(pos)
+            pos += int(w.seg_span[c])
+    w = synth.with_overrides(w, seg_orig_pos0=np.array(new0, np.int32))
+    _, _, plan, dev, res = run_paged(w)
+    lay = oracle.compose_layout(w.req_seg_off, w.seg_row0, w.seg_span, w.seg_orig_pos0,
+                                w.seg_kept_off, w.kept_idx)
+    assert all((d == 0).all() for d in lay["delta"])
+    kp = res["k_pages"].view(torch.int16).cpu().numpy().view(np.uint16)
+    vp = res["v_pages"].view(torch.int16).cpu().numpy().view(np.uint16)
+    bt = plan.block_table()
+    ps = plan.info["page_size"]
+    for b in range(w.batch):
+        rows = lay["src_row"][b]
+        s = np.arange(len(rows))
+        pages = bt[b][s // ps]
+        np.testing.assert_array_equal(kp[pages, :, s % ps, :], w.pool_k[rows])
+        np.testing.assert_array_equal(vp[pages, :, :, s % ps], w.pool_v[rows])
+
+
+# ---------------------------------------------------------------------------
+# launch shapes: split counts and row blocks do not change the result
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("opts", [dict(kv_splits=1), dict(kv_splits=2), dict(kv_splits=7),
+                                  dict(rows_per_block=32), dict(rows_per_block=64),
+                                  dict(rows_per_block=256, kv_splits=3),
+                                  dict(page_size=256)])
+def test_launch_shape_invariance(opts):
+    w = synth.small(batch=2, n_q_heads=16, n_kv_heads=4, suffix_len=45,
+                    keep=("ratio", 0.1, 0.8))
+    _both_paths(w, f"shape {opts}", **opts)
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+
+def test_single_query_token():
+    _both_paths(synth.small(suffix_len=1, batch=2), "S=1")
+
+
+def test_nothing_kept():
+    """No cached slot at all: attention over the causal suffix only."""
+    _both_paths(synth.small(keep=("none",), prefix_len=0, batch=2), "nothing kept")
+
+
+def test_one_cached_token():
+    w = synth.small(batch=1, prefix_len=0, chunks_per_req=1, keep=("count", 1), suffix_len=5)
+    _both_paths(w, "one cached token")
+
+
+def test_empty_and_long_requests_in_one_batch():
+    w = synth.small(batch=3, prefix_len=0, chunks_per_req=2, keep=("ratio", 0.5, 1.0))
+    off = w.seg_kept_off.copy()
+    # request 1 keeps nothing: empty its two segments' kept sets
+    s0, s1 = w.req_seg_off[1], w.req_seg_off[2]
+    kept = np.concatenate([w.kept_idx[off[c]:off[c + 1]] for c in range(w.n_segments)
+                           if not (s0 <= c < s1)])
+    sizes = [0 if s0 <= c < s1 else off[c + 1] - off[c] for c in range(w.n_segments)]
+    w = synth.with_overrides(w, kept_idx=kept.astype(np.int32),
+                             seg_kept_off=np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32))
+    _both_paths(w, "empty request in batch")
+
+
+def test_head_dim_64_bf16_and_int8():
+    for dt in ("bf16", "i8"):
+        _both_paths(synth.small(pool_dtype=dt, head_dim=64, batch=2), f"d=64 {dt}")
+
+
+def test_head_dim_128_fp32():
+    _both_paths(synth.small(pool_dtype="f32", head_dim=128, batch=2), "fp32 d=128")
+
+
+def test_repeated_chunks_and_explicit_placement():
+    w = synth.small(batch=1, chunks_per_req=3, n_pool_chunks=3, prefix_len=0, suffix_len=20)
+    w = synth.with_overrides(
+        w, req_seg_off=np.array([0, 3], np.int32), seg_row0=np.array([0, 200, 0], np.int64),
+        seg_span=np.array([200, 200, 200], np.int32),
+        seg_orig_pos0=np.array([0, 0, 7], np.int32),
+        seg_new_pos0=np.array([1000, 50, 5000], np.int32),
+        seg_kept_off=np.array([0, 70, 75, 145], np.int32),
+        kept_idx=np.concatenate([np.arange(0, 140, 2), np.arange(5), np.arange(0, 140, 2)]
+                                ).astype(np.int32))
+    _both_paths(w, "repeated chunk, explicit placement")
+
+
+def test_gqa_groups():
+    for hq, hkv in [(8, 8), (16, 2), (12, 4)]:
+        _both_paths(synth.small(n_q_heads=hq, n_kv_heads=hkv, batch=1), f"Hq={hq} Hkv={hkv}")
+
+
+def test_lse_optional_and_plan_reuse_across_layers():
+    """One plan serves several layers (the kept set is layer-independent); lse may be NULL."""
+    sp = synth.spec(4)
+    sp = synth.Spec(**{**sp.__dict__, "n_pool_chunks": 8, "chunks_per_req": 8})
+    ws = [synth.build(sp, layer=l, seed=7) for l in range(3)]
+    plan = c2kv.Plan.for_workload(ws[0]).upload()
+    for l, w in enumerate(ws):
+        dev = Dev(w)
+        out = dev.out_like()
+        c2kv.c2kv_compose_attend(plan, dev.pool, dev.q, dev.k_suf, dev.v_suf, out, None)
+        torch.cuda.synchronize()
+        ref_out, ref_lse, _ = oracle_ref(w)
+        lse = torch.from_numpy(ref_lse.astype(np.float32))
+        compare(w, out, lse, ref_out, ref_lse, what=f"layer {l}")

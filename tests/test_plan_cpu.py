@@ -1,0 +1,162 @@
+"""Host side of the C ABI, on the CPU: the library loads and exports every call
+include/c2kv.h declares; the plan's kept-token layout equals the oracle's
+bit for bit; bad descriptors are rejected with the documented status codes."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_17715_amd as c2kv
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_exports_every_declared_symbol():
+    hdr = open(os.path.join(ROOT, "include", "c2kv.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    declared = set(re.findall(r"\b(c2kv_[a-z_]+)\s*\(", hdr))
+    assert {"c2kv_compose", "c2kv_attend", "c2kv_compose_attend"} <= declared
+    lib = ctypes.CDLL(c2kv.LIB_PATH)
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+    assert declared == set(c2kv.EXPORTED)
+
+
+def _oracle_layout(w):
+    return oracle.compose_layout(w.req_seg_off, w.seg_row0, w.seg_span, w.seg_orig_pos0,
+                                 w.seg_kept_off, w.kept_idx, w.seg_new_pos0)
+
+
+def _assert_layout_equal(w, plan):
+    lay = _oracle_layout(w)
+    n, e = plan.requests()
+    assert list(n) == list(map(int, lay["composed_len"]))
+    assert list(e) == list(map(int, lay["span_end"]))
+    src, pos, dl = plan.slots()
+    np.testing.assert_array_equal(src, np.concatenate(lay["src_row"]) if len(src) else src)
+    np.testing.assert_array_equal(pos, np.concatenate(lay["p_new"]) if len(pos) else pos)
+    np.testing.assert_array_equal(dl, np.concatenate(lay["delta"]) if len(dl) else dl)
+
+
+@pytest.mark.parametrize("idx", [1, 2, 4, 5])
+def test_layout_bit_exact_configs(idx):
+    w = synth.config(idx)
+    _assert_layout_equal(w, c2kv.Plan.for_workload(w))
+
+
+def test_layout_bit_exact_ragged_and_edges():
+    for kw in [dict(keep=("ratio", 0.0, 0.4), batch=4, chunks_per_req=5, prefix_len=0),
+               dict(keep=("c2", 4), batch=2),
+               dict(keep=("none",), batch=2, prefix_len=3),
+               dict(keep=("all",), batch=1, chunk_len=65)]:
+        w = synth.small(**kw)
+        _assert_layout_equal(w, c2kv.Plan.for_workload(w))
+
+
+def test_layout_explicit_placement_and_repeats():
+    w = synth.small(batch=1, chunks_per_req=3, n_pool_chunks=3, prefix_len=0)
+    # place the same chunk twice, with a gap, and one segment before another's span end
+    w = synth.with_overrides(
+        w, req_seg_off=np.array([0, 3], np.int32), seg_row0=np.array([0, 200, 0], np.int64),
+        seg_span=np.array([200, 200, 200], np.int32),
+        seg_orig_pos0=np.array([0, 0, 7], np.int32),
+        seg_new_pos0=np.array([1000, 50, 5000], np.int32),
+        seg_kept_off=np.array([0, 3, 5, 8], np.int32),
+        kept_idx=np.array([0, 10, 199, 3, 4, 0, 10, 199], np.int32))
+    plan = c2kv.Plan.for_workload(w)
+    _assert_layout_equal(w, plan)
+    n, e = plan.requests()
+    assert e[0] == 5200
+
+
+def test_block_table_pages():
+    w = synth.small(batch=3, keep=("ratio", 0.2, 0.9))
+    for ps in (64, 128, 256):
+        plan = c2kv.Plan.for_workload(w, page_size=ps)
+        n, _ = plan.requests()
+        bt = plan.block_table()
+        used = []
+        for b in range(len(n)):
+            need = -(-int(n[b]) // ps)
+            row = bt[b]
+            assert all(row[:need] >= 0) and all(row[need:] == -1)
+            used += list(row[:need])
+        assert sorted(used) == list(range(plan.info["n_pages"]))
+
+
+def test_workspace_and_work_list_sizes():
+    for idx in (1, 2, 4, 5):
+        w = synth.config(idx)
+        plan = c2kv.Plan.for_workload(w)
+        i = plan.info
+        assert i["workspace_bytes"] > 0 and i["workspace_bytes"] % 256 == 0
+        assert i["n_work_items"] >= i["n_merge_groups"]
+        assert i["rows_per_block"] in (32, 64, 128, 256)
+    # forced split count is honoured
+    w = synth.config(2)
+    assert c2kv.Plan.for_workload(w, kv_splits=1).info["n_merge_groups"] == 0
+    assert c2kv.Plan.for_workload(w, kv_splits=3).info["max_splits"] == 3
+
+
+def _expect_status(status, fn):
+    with pytest.raises(c2kv.C2KVError) as ei:
+        fn()
+    assert ei.value.status == status, str(ei.value)
+
+
+def test_validation_errors():
+    w = synth.small(batch=1)
+
+    def mk(**kw):
+        args = dict(n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim,
+                    act_dtype=w.act_dtype, rope_base=w.rope_base, req_seg_off=w.req_seg_off,
+                    seg_row0=w.seg_row0, seg_span=w.seg_span, seg_orig_pos0=w.seg_orig_pos0,
+                    seg_kept_off=w.seg_kept_off, kept_idx=w.kept_idx, suffix_len=w.suffix_len)
+        args.update(kw)
+        return lambda: c2kv.Plan(**args)
+
+    mk()()  # the baseline is valid
+    E = c2kv
+    _expect_status(E.C2KV_E_INVAL, mk(n_q_heads=7))
+    _expect_status(E.C2KV_E_UNSUPPORTED, mk(head_dim=96))
+    _expect_status(E.C2KV_E_INVAL, mk(head_dim=63))
+    _expect_status(E.C2KV_E_INVAL, mk(suffix_len=0))
+    _expect_status(E.C2KV_E_INVAL, mk(rope_base=-1.0))
+    _expect_status(E.C2KV_E_INVAL, mk(page_size=100))
+    _expect_status(E.C2KV_E_INVAL, mk(rows_per_block=48))
+    bad = w.kept_idx.copy()
+    bad[0], bad[1] = bad[1], bad[0]
+    _expect_status(E.C2KV_E_INVAL, mk(kept_idx=bad))                  # not ascending
+    bad = w.kept_idx.copy()
+    bad[w.seg_kept_off[1] - 1] = w.seg_span[0]
+    _expect_status(E.C2KV_E_INVAL, mk(kept_idx=bad))                  # outside the span
+    row0 = w.seg_row0.copy()
+    row0[0] = -5
+    _expect_status(E.C2KV_E_INVAL, mk(seg_row0=row0))
+    off = w.req_seg_off.copy()
+    off[-1] += 1
+    _expect_status(E.C2KV_E_INVAL, mk(req_seg_off=off))
+    _expect_status(E.C2KV_E_INVAL,
+                   mk(seg_new_pos0=np.full(len(w.seg_row0), 2**31 - 10, np.int32)))
+    row0 = w.seg_row0.copy()
+    row0[-1] = 2**31
+    _expect_status(E.C2KV_E_UNSUPPORTED, mk(seg_row0=row0))
+
+
+def test_calls_need_an_uploaded_plan():
+    w = synth.small(batch=1)
+    plan = c2kv.Plan.for_workload(w)
+    lib = c2kv.lib()
+    st = lib.c2kv_attend(plan.handle, None, None, None, None, None, None, None, None)
+    assert st == c2kv.C2KV_E_STATE
+    assert b"upload" in lib.c2kv_last_error()
+    st = lib.c2kv_plan_upload(plan.handle, None, 0, None)
+    assert st == c2kv.C2KV_E_WORKSPACE
+    st = lib.c2kv_plan_upload(plan.handle, ctypes.c_void_p(256), 16, None)
+    assert st == c2kv.C2KV_E_WORKSPACE                              # too small
+    st = lib.c2kv_plan_upload(plan.handle, ctypes.c_void_p(100), 1 << 40, None)
+    assert st == c2kv.C2KV_E_WORKSPACE                              # misaligned
