@@ -1,0 +1,347 @@
+"""Benchmark of the C2KV compose-and-attend hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload llama3-8b-layer-bf16]
+
+A step is one pass of the path over one layer of a synthetic workload:
+c2kv_compose_attend (gather, decode, re-rotate, suffix RoPE, split-K attention
+and merge) for the short-suffix workloads, c2kv_compose then c2kv_attend for
+the long-suffix one.  The plan (host layout, built once per batch of requests
+and shared by all layers) is built and uploaded before the timed region.
+
+Inputs live in HBM before timing starts.  Steps rotate over enough device
+copies of the inputs that their footprint exceeds twice the 256 MB Infinity
+Cache, so small workloads are timed against HBM rather than the cache.  The K
+timed steps are replayed from a HIP graph (captured once over the copies);
+an eager run with per-kernel HIP events gives the dominant kernel's average
+duration for the roofline fraction.
+
+Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "composed KV tokens attended/sec per layer + % HBM/MFMA roofline, 1 MI355X"
+PEAK_HBM_GBS = 8000.0           # MI355X HBM3E, GB/s
+PEAK_BF16_TFLOPS = 2500.0       # dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3        # fp32 (MFMA / packed vector)
+MALL_BYTES = 256 << 20
+
+WORKLOADS = {
+    "tiny-fp32": 1,
+    "llama3-8b-layer-bf16": 2,
+    "ragged-batch-bf16": 3,
+    "int8-32layer": 4,
+    "70b-long-suffix-bf16": 5,
+}
+DEFAULT_WORKLOAD = "llama3-8b-layer-bf16"
+LONG_SUFFIX = {"70b-long-suffix-bf16"}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_work(w, composed: np.ndarray):
+    """Bytes and flops the method must move / compute for one layer (per launch
+    of the attention kernel), excluding unread pool rows and masked pairs.
+
+    bytes per composed token: K and V rows of one token (2 H_kv D b_kv), the
+      int8 scales (2 H_kv 4) and the slot index (4);
+    bytes per suffix token: q and out (2 H_q D b_act), suffix k and v
+      (2 H_kv D b_act), lse (4 H_q);
+    flops: 4 H_q D per visible (query, key) pair (Q K^T and P V)."""
+    Hq, Hkv, D, S, B = w.n_q_heads, w.n_kv_heads, w.head_dim, w.suffix_len, w.batch
+    b_kv = {"f32": 4, "bf16": 2, "i8": 1}[w.pool_dtype]
+    b_act = {"f32": 4, "bf16": 2}[w.act_dtype]
+    n_tok = int(composed.sum())
+    per_tok = 2 * Hkv * D * b_kv + (8 * Hkv if w.pool_dtype == "i8" else 0) + 4
+    per_q = 2 * Hq * D * b_act + 2 * Hkv * D * b_act + 4 * Hq
+    byts = n_tok * per_tok + B * S * per_q
+    pairs = n_tok * S + B * S * (S + 1) // 2
+    flops = 4 * Hq * D * pairs
+    return dict(bytes=int(byts), flops=int(flops), bytes_per_token=per_tok,
+                bytes_per_query=per_q, pairs=int(pairs), tokens=n_tok)
+
+
+def paged_attend_bytes(w, composed):
+    """Attention over materialised pages reads act-dtype K/V rows."""
+    b_act = {"f32": 4, "bf16": 2}[w.act_dtype]
+    Hq, Hkv, D, S, B = w.n_q_heads, w.n_kv_heads, w.head_dim, w.suffix_len, w.batch
+    n_tok = int(composed.sum())
+    per_q = 2 * Hq * D * b_act + 2 * Hkv * D * b_act + 4 * Hq
+    return n_tok * (2 * Hkv * D * b_act + 4) + B * S * per_q
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "plan.cpp", "api.cpp"):
+        with open(os.path.join(ROOT, "paper_2607_17715_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str, kernel: str, n_launch_bytes: float):
+    """HBM traffic per launch from the committed rocprofv3 counter summary, or
+    None when there is none or the kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("source_sha") != kernel_source_sha():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, idx: int):
+    """The float64 oracle timed on this host on a bounded sample of the workload."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    lay = oracle.compose_layout(w.req_seg_off, w.seg_row0, w.seg_span, w.seg_orig_pos0,
+                                w.seg_kept_off, w.kept_idx, w.seg_new_pos0)
+    N = int(lay["composed_len"].sum())
+    S = w.suffix_len
+    if idx in (1, 2, 4):
+        # whole layer, repeated for about 10 s
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oracle.compose_attend(w)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el > 10.0 or reps >= 200:
+                break
+        per_layer = el / reps
+        sample = f"whole layer x{reps} (compose of {N} slots + attention of all {S} suffix tokens)"
+    else:
+        # compose every kept token of the first request(s), attention of a few suffix rows,
+        # scaled to the whole layer
+        reqs = list(range(min(w.batch, 2)))
+        rows = list(range(0, S, max(1, S // 8)))[:8]
+        t0 = time.perf_counter()
+        oracle.compose_attend(w, rows=rows, requests=reqs)
+        el = time.perf_counter() - t0
+        frac_req = float(lay["composed_len"][reqs].sum() + len(reqs)) / float(N + w.batch)
+        per_layer = el / frac_req * (S / len(rows))
+        sample = (f"requests {reqs} ({int(lay['composed_len'][reqs].sum())} slots composed), "
+                  f"{len(rows)} of {S} suffix rows; scaled by suffix rows and by slots")
+    return {"value": N / per_layer, "unit": "tokens/s/layer", "cores": int(threads),
+            "kind": "oracle", "sample": sample, "seconds_per_layer": per_layer}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1024)
+    ap.add_argument("--warmup", type=int, default=32)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
+    ap.add_argument("--copies", type=int, default=0, help="input copies to rotate over (0: auto)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--kv-splits", type=int, default=0)
+    ap.add_argument("--rows-per-block", type=int, default=0)
+    ap.add_argument("--merge-mode", type=int, default=0)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one device copy of this many MiB first (counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the compose-and-attend path here runs on a single "
+              "MI355X (--gpus 1); multi-GPU sharding is described in DESIGN.md, not built.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_17715_amd as c2kv
+    import synth
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {n} bytes done")
+        del src, dst
+
+    idx = WORKLOADS[args.workload]
+    log(f"workload {args.workload}: generating inputs")
+    w = synth.config(idx)
+    plan = c2kv.Plan.for_workload(w, kv_splits=args.kv_splits,
+                                  rows_per_block=args.rows_per_block,
+                                  merge_mode=args.merge_mode).upload()
+    composed, span_end = plan.requests()
+    work = algorithmic_work(w, composed)
+    long_suffix = args.workload in LONG_SUFFIX
+    act = torch.float32 if w.act_dtype == "f32" else torch.bfloat16
+
+    # ---- device inputs, replicated so the rotation spans > 2x the Infinity Cache
+    base = dict(k=c2kv.to_device(w.pool_k, w.pool_dtype), v=c2kv.to_device(w.pool_v, w.pool_dtype),
+                ks=None if w.pool_k_scale is None else c2kv.to_device(w.pool_k_scale, "f32"),
+                vs=None if w.pool_v_scale is None else c2kv.to_device(w.pool_v_scale, "f32"),
+                q=c2kv.to_device(w.q, w.act_dtype), k_suf=c2kv.to_device(w.k_suf, w.act_dtype),
+                v_suf=c2kv.to_device(w.v_suf, w.act_dtype))
+    footprint = sum(t.numel() * t.element_size() for t in base.values() if t is not None)
+    copies = args.copies or int(min(64, max(2, math.ceil(2.2 * MALL_BYTES / footprint))))
+    log(f"footprint {footprint / 1e6:.1f} MB per copy, {copies} copies")
+    sets = [base] + [{k: (None if t is None else t.clone()) for k, t in base.items()}
+                     for _ in range(copies - 1)]
+    for s in sets:
+        s["pool"] = c2kv.pool_desc(s["k"], s["v"], s["ks"], s["vs"])
+        s["out"] = torch.empty_like(s["q"])
+        s["lse"] = torch.empty((w.batch, w.n_q_heads, w.suffix_len), dtype=torch.float32,
+                               device="cuda")
+    if long_suffix:
+        ksh, vsh = c2kv.page_shapes(plan)
+        kp = torch.empty(ksh, dtype=act, device="cuda")
+        vp = torch.empty(vsh, dtype=act, device="cuda")
+
+    def step(i):
+        s = sets[i % copies]
+        if long_suffix:
+            c2kv.c2kv_compose(plan, s["pool"], kp, vp)
+            c2kv.c2kv_attend(plan, kp, vp, s["q"], s["k_suf"], s["v_suf"], s["out"], s["lse"])
+        else:
+            c2kv.c2kv_compose_attend(plan, s["pool"], s["q"], s["k_suf"], s["v_suf"], s["out"],
+                                     s["lse"])
+
+    # ---- warmup (eager)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    assert torch.isfinite(sets[0]["out"]).all().item(), "non-finite output"
+
+    K = args.steps
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    # ---- eager timing (reported beside the graph number)
+    ke = min(K, 256)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(ke):
+        step(i)
+    end.record()
+    torch.cuda.synchronize()
+    eager_ms = start.elapsed_time(end) / ke
+
+    # ---- timed region: K steps replayed from graphs captured over the copies
+    graph_used = not args.no_graph
+    if graph_used:
+        n_full, rem = divmod(K, copies)
+        g_full = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_full):
+            for i in range(copies):
+                step(i)
+        g_rem = None
+        if rem:
+            g_rem = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_rem):
+                for i in range(rem):
+                    step(i)
+        g_full.replay()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(n_full):
+            g_full.replay()
+        if g_rem is not None:
+            g_rem.replay()
+        end.record()
+        torch.cuda.synchronize()
+        total_ms = start.elapsed_time(end)
+    else:
+        torch.cuda.synchronize()
+        start.record()
+        for i in range(K):
+            step(i)
+        end.record()
+        torch.cuda.synchronize()
+        total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / K
+    value = work["tokens"] / (ms_per_step * 1e-3)
+
+    # ---- per-kernel durations (HIP events around each launch, on its stream)
+    c2kv.timing_reset()
+    c2kv.timing_enable(True)
+    for i in range(ke):
+        step(i)
+    torch.cuda.synchronize()
+    c2kv.timing_enable(False)
+    kern = {}
+    for name in ("compose", "attn_paged", "attn_pool", "merge"):
+        ms, n = c2kv.timing_read(name)
+        if n:
+            kern[name] = {"avg_us": 1e3 * ms / n, "launches": n}
+    c2kv.timing_reset()
+
+    dom = "attn_paged" if long_suffix else "attn_pool"
+    dom_s = kern[dom]["avg_us"] * 1e-6
+    mfma_bound = idx in (3, 5)
+    if mfma_bound:
+        peak = PEAK_FP32_TFLOPS if w.act_dtype == "f32" else PEAK_BF16_TFLOPS
+        achieved = work["flops"] / dom_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                "frac": achieved / peak}
+        dom_bytes = paged_attend_bytes(w, composed) if long_suffix else work["bytes"]
+    else:
+        dom_bytes = work["bytes"]
+        achieved = dom_bytes / dom_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+    roof["traffic"] = load_traffic(args.workload, dom, dom_bytes)
+    roof["kernel"] = dom
+    roof["kernel_avg_us"] = kern[dom]["avg_us"]
+    roof["algorithmic_bytes"] = dom_bytes
+    roof["algorithmic_flops"] = work["flops"]
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s/layer",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.act_dtype == "f32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "n_q_heads": w.n_q_heads,
+                   "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "pool_dtype": w.pool_dtype, "batch": w.batch, "suffix_len": w.suffix_len,
+                   "composed_tokens": work["tokens"],
+                   "path": "compose+attend" if long_suffix else "compose_attend",
+                   "plan": {**{k: plan.info[k] for k in ("rows_per_block", "n_work_items",
+                                                         "n_merge_groups", "max_splits")},
+                            "merge_mode": args.merge_mode},
+                   "input_copies": copies, "graph": graph_used},
+        "roofline": roof,
+        "kernels_us": kern,
+        "eager_ms_per_step": eager_ms,
+        "source_sha": kernel_source_sha(),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the float64 oracle on the host (cpu_baseline)")
+        result["cpu_baseline"] = cpu_baseline(w, idx)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -52,7 +52,8 @@ class ComposeDesc(ctypes.Structure):
 
 class PlanOpts(ctypes.Structure):
     _fields_ = [("page_size", ctypes.c_int32), ("kv_splits", ctypes.c_int32),
-                ("rows_per_block", ctypes.c_int32), ("num_cus", ctypes.c_int32)]
+                ("rows_per_block", ctypes.c_int32), ("num_cus", ctypes.c_int32),
+                ("merge_mode", ctypes.c_int32)]
 
 
 class PoolDesc(ctypes.Structure):
@@ -148,7 +149,7 @@ class Plan:
                  rope_base: float, req_seg_off, seg_row0, seg_span, seg_orig_pos0,
                  seg_kept_off, kept_idx, suffix_len: int, seg_new_pos0=None,
                  softmax_scale: float = 0.0, page_size: int = 0, kv_splits: int = 0,
-                 rows_per_block: int = 0, num_cus: int = 0):
+                 rows_per_block: int = 0, num_cus: int = 0, merge_mode: int = 0):
         self._arrays = dict(
             req_seg_off=np.ascontiguousarray(req_seg_off, np.int32),
             seg_row0=np.ascontiguousarray(seg_row0, np.int64),
@@ -167,7 +168,7 @@ class Plan:
                            _np_ptr(a["seg_span"]), _np_ptr(a["seg_orig_pos0"]),
                            _np_ptr(a["seg_new_pos0"]), _np_ptr(a["seg_kept_off"]),
                            _np_ptr(a["kept_idx"]))
-        opts = PlanOpts(page_size, kv_splits, rows_per_block, num_cus)
+        opts = PlanOpts(page_size, kv_splits, rows_per_block, num_cus, merge_mode)
         h = ctypes.c_void_p()
         _check(_lib.c2kv_plan_create(ctypes.byref(self.cfg), ctypes.byref(desc),
                                      int(suffix_len), ctypes.byref(opts), ctypes.byref(h)))

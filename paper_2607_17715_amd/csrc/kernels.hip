@@ -142,19 +142,79 @@ template <> struct Mma<__bf16> {
 };
 
 // ----------------------------------------------------------------------------
+// raw 32-bit words of 8 consecutive elements (2 * sizeof(S) words)
+// ----------------------------------------------------------------------------
+
+template <typename S>
+__device__ inline void raw_load8(uint32_t* w, const S* p) {
+  if constexpr (sizeof(S) == 4) {
+    const uint4 u0 = *reinterpret_cast<const uint4*>(p);
+    const uint4 u1 = *reinterpret_cast<const uint4*>(p + 4);
+    w[0] = u0.x; w[1] = u0.y; w[2] = u0.z; w[3] = u0.w;
+    w[4] = u1.x; w[5] = u1.y; w[6] = u1.z; w[7] = u1.w;
+  } else if constexpr (sizeof(S) == 2) {
+    const uint4 u0 = *reinterpret_cast<const uint4*>(p);
+    w[0] = u0.x; w[1] = u0.y; w[2] = u0.z; w[3] = u0.w;
+  } else {
+    const uint2 u0 = *reinterpret_cast<const uint2*>(p);
+    w[0] = u0.x; w[1] = u0.y;
+  }
+}
+template <typename S>
+__device__ inline void raw_zero8(uint32_t* w) {
+#pragma unroll
+  for (int i = 0; i < 2 * int(sizeof(S)); ++i) w[i] = 0u;
+}
+template <typename S>
+__device__ inline void raw_to_f8(const uint32_t* w, float (&x)[8]) {
+  if constexpr (sizeof(S) == 4) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = __uint_as_float(w[i]);
+  } else if constexpr (sizeof(S) == 2) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      x[i] = static_cast<float>(static_cast<int8_t>((w[i >> 2] >> (8 * (i & 3))) & 0xffu));
+  }
+}
+
+// zero the elements [n_keep, 16 / sizeof(T)) of a 16-byte vector
+template <typename T>
+__device__ inline uint4 keep_first(uint4 v, int n_keep) {
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  constexpr int EPW = 4 / sizeof(T);              // elements per word
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if constexpr (EPW == 1) {
+      if (i >= n_keep) w[i] = 0u;
+    } else {
+      if (2 * i >= n_keep) w[i] = 0u;
+      else if (2 * i + 1 >= n_keep) w[i] &= 0x0000ffffu;
+    }
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// ----------------------------------------------------------------------------
 // parameters
 // ----------------------------------------------------------------------------
 
 struct AttnParams {
-  int Hq, Hkv, G, S, PS, max_pages, RB;
+  int Hq, Hkv, G, S, PS, max_pages, RB, n_seg, merge_in_kernel;
   float qscale;                 // softmax scale * log2(e)
   const int* req_slot0;
-  const int* slot_src;
-  const int* slot_seg;
-  const float2* seg_cs;
-  const float2* suf_cs;
+  const int2* slot_info;        // (pool row, segment) per composed slot
+  const float2* seg_cs;         // [n_seg][D/2] cos/sin(delta * theta_i)
+  const float2* suf_cs;         // [B][S][D/2]  cos/sin((span_end + t) * theta_i)
   const int* block_table;
   const WorkItem* items;
+  const MergeGroup* merges;
+  int* counters;                // [n_merge], zero between launches
   const void* k;                // pages or pool
   const void* v;
   const float* k_scale;
@@ -171,8 +231,7 @@ struct AttnParams {
 struct ComposeParams {
   int Hkv, PS, max_pages;
   const int* req_slot0;
-  const int* slot_src;
-  const int* slot_seg;
+  const int2* slot_info;
   const int* slot_pos;
   const float2* seg_cs;
   const int* block_table;
@@ -196,94 +255,78 @@ struct MergeParams {
   float* lse;
 };
 
-// ----------------------------------------------------------------------------
-// tile loaders: fill sK[KT][D + pad] (keys at final positions) and
-// sV[D][KT + pad] (values transposed); keys >= nvalid are zero-filled.
-// ----------------------------------------------------------------------------
-
 template <typename T, int D>
 struct Lds {
   static constexpr int PAD = 16 / sizeof(T);
-  static constexpr int LDK = D + PAD;
-  static constexpr int LDV = KT + PAD;
+  static constexpr int LDK = D + PAD;       // sK[KT][LDK]: keys at final positions
+  static constexpr int LDV = KT + PAD;      // sV[D][LDV]: values transposed
 };
 
-// keys from one row per key (pool or suffix), turned by a per-key cos/sin row
-// and decoded with an optional per-key scale; values transposed into sV.
-template <typename T, int D, typename Src, typename RowFn>
-__device__ inline void load_rows_tile(T* sK, T* sV, int nvalid, RowFn row_of) {
-  using L = Lds<T, D>;
-  constexpr int KU = D / 16;                // (chunk, chunk + D/2) pairs per key
-  for (int u = threadIdx.x; u < KT * KU; u += blockDim.x) {
-    const int kk = u / KU, c = u % KU;
-    T* dst = sK + kk * L::LDK + 8 * c;
-    if (kk < nvalid) {
-      const Src* kp; const Src* vp; float ks, vs; const float2* cs;
-      row_of(kk, kp, vp, ks, vs, cs);
-      float x[8], y[8], cc[8], ss[8];
-      load8(kp + 8 * c, x);
-      load8(kp + 8 * c + D / 2, y);
-      if constexpr (sizeof(Src) == 1) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) { x[e] *= ks; y[e] *= ks; }
-      }
-      load_cs8(cs + 8 * c, cc, ss);
-      rotate8(x, y, cc, ss);
-      store8(dst, x);
-      store8(dst + D / 2, y);
-    } else {
-      store8_zero(dst);
-      store8_zero(dst + D / 2);
-    }
-  }
-  constexpr int VU = D / 8;                 // 8-element chunks per key
-  for (int u = threadIdx.x; u < KT * VU; u += blockDim.x) {
-    const int c = u / KT, kk = u % KT;
-    float x[8];
-    if (kk < nvalid) {
-      const Src* kp; const Src* vp; float ks, vs; const float2* cs;
-      row_of(kk, kp, vp, ks, vs, cs);
-      load8(vp + 8 * c, x);
-      if constexpr (sizeof(Src) == 1) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] *= vs;
-      }
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = 0.f;
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) sV[(8 * c + e) * L::LDV + kk] = from_f<T>(x[e]);
-  }
-}
+constexpr int NSEG = 4;   // segments whose cos/sin a key tile caches in LDS
 
-// keys and transposed values straight from a page (already composed)
+constexpr int imax(int a, int b) { return a > b ? a : b; }
+
+// Per-thread work of one key tile for an NT-thread workgroup.
+template <typename T, typename PoolT, int D, int NT, bool PAGED>
+struct Shape {
+  static constexpr int KU_TOT = KT * (D / 16);   // key units: (chunk, chunk + D/2) pairs
+  static constexpr int VU_TOT = KT * (D / 8);    // value units: 8-element chunks
+  static constexpr int NKU = (KU_TOT + NT - 1) / NT;
+  static constexpr int NVU = (VU_TOT + NT - 1) / NT;
+  static constexpr int EPV = 16 / sizeof(T);     // elements per 16-byte vector
+  static constexpr int PK_TOT = KT * D / EPV;    // page vectors, keys
+  static constexpr int PV_TOT = D * KT / EPV;    // page vectors, transposed values
+  static constexpr int NPK = (PK_TOT + NT - 1) / NT;
+  static constexpr int NPV = (PV_TOT + NT - 1) / NT;
+  static constexpr int WP = 2 * int(sizeof(PoolT));  // words per 8 pool elements
+  static constexpr int WA = 2 * int(sizeof(T));      // words per 8 act elements
+  static constexpr int RKW = imax(NKU * 2 * WA, PAGED ? NPK * 4 : NKU * 2 * WP);
+  static constexpr int RVW = imax(NVU * WA, PAGED ? NPV * 4 : NVU * WP);
+  static constexpr int CS_TOT = NSEG * (D / 2);
+  static constexpr int NCS = (CS_TOT + NT - 1) / NT;
+};
+
+// ----------------------------------------------------------------------------
+// log-sum-exp combine of the key splits of one row block (rows [rlo, rhi))
+// ----------------------------------------------------------------------------
+
 template <typename T, int D>
-__device__ inline void load_paged_tile(T* sK, T* sV, const T* kpage, const T* vpage,
-                                       int PS, int nvalid) {
-  using L = Lds<T, D>;
-  constexpr int EPV = 16 / sizeof(T);       // elements per 16-byte vector
-  constexpr int KV = D / EPV;               // vectors per key row
-  for (int u = threadIdx.x; u < KT * KV; u += blockDim.x) {
-    const int kk = u / KV, vec = u % KV;
-    uint4 val = make_uint4(0u, 0u, 0u, 0u);
-    if (kk < nvalid) val = *reinterpret_cast<const uint4*>(kpage + size_t(kk) * D + vec * EPV);
-    *reinterpret_cast<uint4*>(sK + kk * L::LDK + vec * EPV) = val;
-  }
-  constexpr int VV = KT / EPV;              // vectors per transposed value row
-  for (int u = threadIdx.x; u < D * VV; u += blockDim.x) {
-    const int d = u / VV, vec = u % VV;
-    uint4 val = make_uint4(0u, 0u, 0u, 0u);
-    const int k0 = vec * EPV;
-    if (k0 + EPV <= nvalid) {
-      val = *reinterpret_cast<const uint4*>(vpage + size_t(d) * PS + k0);
-    } else if (k0 < nvalid) {
-      T tmp[EPV];
-#pragma unroll
-      for (int e = 0; e < EPV; ++e) tmp[e] = (k0 + e < nvalid) ? vpage[size_t(d) * PS + k0 + e] : from_f<T>(0.f);
-      val = *reinterpret_cast<const uint4*>(tmp);
+__device__ inline void merge_rows(const MergeGroup& mg, int rlo, int rhi, const float* part_o,
+                                  const float* part_lse, int RB, int Hq, int G, int S,
+                                  void* out, float* lse, int tid, int nthr) {
+  constexpr int TPR = D / 4;
+  for (int idx = tid; idx < (rhi - rlo) * TPR; idx += nthr) {
+    const int rloc = rlo + idx / TPR;
+    const int d = 4 * (idx % TPR);
+    const float* pl = part_lse + size_t(mg.part0) * RB + rloc;
+    const float* po = part_o + (size_t(mg.part0) * RB + rloc) * D + d;
+    float mx = kNegInf;
+#pragma unroll 8
+    for (int i = 0; i < mg.nsplit; ++i) mx = fmaxf(mx, pl[size_t(i) * RB]);
+    float z = 0.f;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+    for (int i = 0; i < mg.nsplit; ++i) {
+      const float li = pl[size_t(i) * RB];
+      const float w = (li == kNegInf) ? 0.f : __expf(li - mx);
+      const float4 v = *reinterpret_cast<const float4*>(po + size_t(i) * RB * D);
+      z += w;
+      acc.x += w * v.x; acc.y += w * v.y; acc.z += w * v.z; acc.w += w * v.w;
     }
-    *reinterpret_cast<uint4*>(sV + d * L::LDV + k0) = val;
+    const float inv = z > 0.f ? 1.f / z : 0.f;
+    const int r = mg.row0 + rloc;
+    const int t = r / G, h = mg.g * G + r % G;
+    T* orow = static_cast<T*>(out) + ((size_t(mg.b) * S + t) * Hq + h) * D;
+    if constexpr (sizeof(T) == 4) {
+      *reinterpret_cast<float4*>(orow + d) =
+          make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+    } else {
+      uint2 u;
+      u.x = pack_bf16(acc.x * inv, acc.y * inv);
+      u.y = pack_bf16(acc.z * inv, acc.w * inv);
+      *reinterpret_cast<uint2*>(orow + d) = u;
+    }
+    if (lse && d == 0) lse[(size_t(mg.b) * Hq + h) * S + t] = z > 0.f ? mx + __logf(z) : kNegInf;
   }
 }
 
@@ -291,30 +334,37 @@ __device__ inline void load_paged_tile(T* sK, T* sV, const T* kpage, const T* vp
 // attention
 // ----------------------------------------------------------------------------
 
-template <typename T, int D, int SRC>
-__global__ __launch_bounds__(512) void attn_kernel(AttnParams a) {
+template <typename T, int D, int SRC, int NT>
+__global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   using M = Mma<T>;
   using Op = typename M::Op;
   using L = Lds<T, D>;
   using PoolT = typename std::conditional<SRC == SRC_POOL_I8, int8_t, T>::type;
+  constexpr bool kPaged = SRC == SRC_PAGED;
+  using Sh = Shape<T, PoolT, D, NT, kPaged>;
   constexpr int KPL = M::KPL;
   constexpr int KSTEP = 2 * KPL;            // contraction length of one MFMA
   constexpr int NQC = D / KSTEP;            // Q operand chunks over d
   constexpr int NDB = D / 32;               // 32-wide d blocks of the output
   constexpr int CPB = 32 / KSTEP;           // P*V chunks per 32-key block
   constexpr int NPC = KT / KSTEP;           // P*V chunks per key tile
+  constexpr int HALF = D / 2;
+  constexpr int KUPK = D / 16;              // key units per key
 
   __shared__ __attribute__((aligned(16))) T sK[KT * L::LDK];
   __shared__ __attribute__((aligned(16))) T sV[D * L::LDV];
+  __shared__ __attribute__((aligned(16))) float2 sCS[kPaged ? 2 : Sh::CS_TOT];
+  __shared__ int s_last;
 
+  const int tid = threadIdx.x;
   const WorkItem it = a.items[blockIdx.x];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = tid >> 6, lane = tid & 63;
   const int qi = lane & 31, half = lane >> 5;
   const int b = it.b, g = it.g;
+  const int S = a.S, G = a.G;
   const int slot0 = a.req_slot0[b];
   const int N = a.req_slot0[b + 1] - slot0;
   const int nct = (N + KT - 1) / KT;
-  const int S = a.S, G = a.G;
 
   const int rloc = wave * 32 + qi;
   const bool row_ok = rloc < it.nrows;
@@ -328,31 +378,282 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnParams a) {
   Op qop[NQC];
   {
     const T* qrow = static_cast<const T*>(a.q) + ((size_t(b) * S + t) * a.Hq + h) * D;
-    const float2* cs = a.suf_cs + (size_t(b) * S + t) * (D / 2);
+    const float2* cs = a.suf_cs + (size_t(b) * S + t) * HALF;
 #pragma unroll
     for (int c = 0; c < NQC / 2; ++c) {
+      const int d0 = c * KSTEP + half * KPL;
+      float x[KPL], y[KPL], cc[KPL], ss[KPL];
+      if (row_ok) {
+        if constexpr (KPL == 8) {
+          uint32_t wx[4], wy[4];
+          raw_load8<T>(wx, qrow + d0);
+          raw_load8<T>(wy, qrow + d0 + HALF);
+          float fx[8], fy[8];
+          raw_to_f8<T>(wx, fx);
+          raw_to_f8<T>(wy, fy);
+          float c8[8], s8[8];
+          load_cs8(cs + d0, c8, s8);
 #pragma unroll
-      for (int e = 0; e < KPL; ++e) {
-        const int d = c * KSTEP + half * KPL + e;
-        float x = 0.f, y = 0.f;
-        if (row_ok) {
-          x = to_f(qrow[d]);
-          y = to_f(qrow[d + D / 2]);
-          const float2 w = cs[d];
-          rotate_pair(x, y, w.x, w.y);
-          x *= a.qscale;
-          y *= a.qscale;
-        }
-        if constexpr (KPL == 1) {
-          qop[c] = x;
-          qop[c + NQC / 2] = y;
+          for (int e = 0; e < 8; ++e) { x[e] = fx[e]; y[e] = fy[e]; cc[e] = c8[e]; ss[e] = s8[e]; }
         } else {
-          qop[c][e] = from_f<T>(x);
-          qop[c + NQC / 2][e] = from_f<T>(y);
+          x[0] = to_f(qrow[d0]);
+          y[0] = to_f(qrow[d0 + HALF]);
+          const float2 w = cs[d0];
+          cc[0] = w.x;
+          ss[0] = w.y;
+        }
+#pragma unroll
+        for (int e = 0; e < KPL; ++e) {
+          rotate_pair(x[e], y[e], cc[e], ss[e]);
+          x[e] *= a.qscale;
+          y[e] *= a.qscale;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < KPL; ++e) { x[e] = 0.f; y[e] = 0.f; }
+      }
+      if constexpr (KPL == 1) {
+        qop[c] = x[0];
+        qop[c + NQC / 2] = y[0];
+      } else {
+#pragma unroll
+        for (int e = 0; e < KPL; ++e) {
+          qop[c][e] = from_f<T>(x[e]);
+          qop[c + NQC / 2][e] = from_f<T>(y[e]);
         }
       }
     }
   }
+
+  // ---- tile pipeline: indices two tiles ahead, data one tile ahead --------
+  uint32_t rk[Sh::RKW], rv[Sh::RVW];
+  int2 nk[Sh::NKU];
+  int2 nv = make_int2(-1, -1);
+  int n_seg0 = 0, n_page = 0;
+  int pk_seg[Sh::NKU];
+  float pk_scale[Sh::NKU];
+  float pv_scale = 1.f;
+  float2 pcs[Sh::NCS];
+  int p_seg0 = 0;
+#pragma unroll
+  for (int i = 0; i < Sh::NKU; ++i) { nk[i] = make_int2(-1, -1); pk_seg[i] = -1; pk_scale[i] = 1.f; }
+#pragma unroll
+  for (int j = 0; j < Sh::NCS; ++j) pcs[j] = make_float2(1.f, 0.f);
+
+  const T* ksuf = static_cast<const T*>(a.k_suf);
+  const T* vsuf = static_cast<const T*>(a.v_suf);
+  const PoolT* kpool = static_cast<const PoolT*>(a.k);
+  const PoolT* vpool = static_cast<const PoolT*>(a.v);
+  const int kkv = tid % KT;                 // the key of this thread's value units
+
+  auto fetch_idx = [&](int tile) {
+    if (tile >= nct) return;                // suffix tiles need no index
+    const int k0 = tile * KT;
+    const int nvalid = min(KT, N - k0);
+    if constexpr (kPaged) {
+      n_page = a.block_table[size_t(b) * a.max_pages + k0 / a.PS];
+    } else {
+#pragma unroll
+      for (int i = 0; i < Sh::NKU; ++i) {
+        const int u = tid + i * NT;
+        const int kk = u / KUPK;
+        nk[i] = make_int2(-1, -1);
+        if (u < Sh::KU_TOT && kk < nvalid) nk[i] = a.slot_info[slot0 + k0 + kk];
+      }
+      nv = make_int2(-1, -1);
+      if (kkv < nvalid) nv = a.slot_info[slot0 + k0 + kkv];
+      n_seg0 = a.slot_info[slot0 + k0].y;
+    }
+  };
+
+  auto fetch_data = [&](int tile) {
+    const bool suffix = tile >= nct;
+    const int k0 = suffix ? (tile - nct) * KT : tile * KT;
+    const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
+    if (suffix) {
+#pragma unroll
+      for (int i = 0; i < Sh::NKU; ++i) {
+        const int u = tid + i * NT;
+        const int kk = u / KUPK, c = u % KUPK;
+        uint32_t* w = rk + i * 2 * Sh::WA;
+        if (u < Sh::KU_TOT && kk < nvalid) {
+          const size_t row = (size_t(b) * S + k0 + kk) * a.Hkv + g;
+          raw_load8<T>(w, ksuf + row * D + 8 * c);
+          raw_load8<T>(w + Sh::WA, ksuf + row * D + 8 * c + HALF);
+        } else {
+          raw_zero8<T>(w);
+          raw_zero8<T>(w + Sh::WA);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < Sh::NVU; ++i) {
+        const int u = tid + i * NT;
+        const int c = u / KT;
+        uint32_t* w = rv + i * Sh::WA;
+        if (u < Sh::VU_TOT && kkv < nvalid) {
+          const size_t row = (size_t(b) * S + k0 + kkv) * a.Hkv + g;
+          raw_load8<T>(w, vsuf + row * D + 8 * c);
+        } else {
+          raw_zero8<T>(w);
+        }
+      }
+    } else if constexpr (kPaged) {
+      constexpr int EPV = Sh::EPV;
+      const size_t ph = size_t(n_page) * a.Hkv + g;
+      const int off = k0 % a.PS;
+      const T* kpage = static_cast<const T*>(a.k) + (ph * a.PS + off) * D;
+      const T* vpage = static_cast<const T*>(a.v) + ph * D * a.PS + off;
+#pragma unroll
+      for (int i = 0; i < Sh::NPK; ++i) {
+        const int u = tid + i * NT;
+        const int kk = u / (D / EPV), vec = u % (D / EPV);
+        uint4 val = make_uint4(0u, 0u, 0u, 0u);
+        if (u < Sh::PK_TOT && kk < nvalid)
+          val = *reinterpret_cast<const uint4*>(kpage + size_t(kk) * D + vec * EPV);
+        rk[4 * i] = val.x; rk[4 * i + 1] = val.y; rk[4 * i + 2] = val.z; rk[4 * i + 3] = val.w;
+      }
+#pragma unroll
+      for (int i = 0; i < Sh::NPV; ++i) {
+        const int u = tid + i * NT;
+        const int d = u / (KT / EPV), vec = u % (KT / EPV);
+        uint4 val = make_uint4(0u, 0u, 0u, 0u);
+        if (u < Sh::PV_TOT && vec * EPV < nvalid)
+          val = *reinterpret_cast<const uint4*>(vpage + size_t(d) * a.PS + vec * EPV);
+        rv[4 * i] = val.x; rv[4 * i + 1] = val.y; rv[4 * i + 2] = val.z; rv[4 * i + 3] = val.w;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < Sh::NKU; ++i) {
+        const int u = tid + i * NT;
+        const int c = u % KUPK;
+        uint32_t* w = rk + i * 2 * Sh::WP;
+        pk_seg[i] = nk[i].y;
+        if (nk[i].x >= 0) {
+          const size_t row = size_t(nk[i].x) * a.Hkv + g;
+          raw_load8<PoolT>(w, kpool + row * D + 8 * c);
+          raw_load8<PoolT>(w + Sh::WP, kpool + row * D + 8 * c + HALF);
+          if constexpr (SRC == SRC_POOL_I8) pk_scale[i] = a.k_scale[row];
+        } else {
+          raw_zero8<PoolT>(w);
+          raw_zero8<PoolT>(w + Sh::WP);
+        }
+      }
+      if (nv.x >= 0) {
+        const size_t row = size_t(nv.x) * a.Hkv + g;
+#pragma unroll
+        for (int i = 0; i < Sh::NVU; ++i) {
+          const int u = tid + i * NT;
+          const int c = u / KT;
+          if (u < Sh::VU_TOT) raw_load8<PoolT>(rv + i * Sh::WP, vpool + row * D + 8 * c);
+          else raw_zero8<PoolT>(rv + i * Sh::WP);
+        }
+        if constexpr (SRC == SRC_POOL_I8) pv_scale = a.v_scale[row];
+      } else {
+#pragma unroll
+        for (int i = 0; i < Sh::NVU; ++i) raw_zero8<PoolT>(rv + i * Sh::WP);
+      }
+      p_seg0 = n_seg0;
+#pragma unroll
+      for (int j = 0; j < Sh::NCS; ++j) {
+        const int e = tid + j * NT;
+        const int seg = n_seg0 + e / HALF;
+        if (e < Sh::CS_TOT && seg < a.n_seg) pcs[j] = a.seg_cs[size_t(seg) * HALF + e % HALF];
+      }
+    }
+  };
+
+  // registers -> LDS (keys turned to their final positions, values transposed)
+  auto commit = [&](int tile) {
+    const bool suffix = tile >= nct;
+    const int k0 = suffix ? (tile - nct) * KT : tile * KT;
+    const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
+    if (suffix || !kPaged) {
+      using RawT = typename std::conditional<kPaged, T, PoolT>::type;
+      const bool from_pool = !suffix;
+#pragma unroll
+      for (int i = 0; i < Sh::NKU; ++i) {
+        const int u = tid + i * NT;
+        if (u >= Sh::KU_TOT) continue;
+        const int kk = u / KUPK, c = u % KUPK;
+        T* dst = sK + kk * L::LDK + 8 * c;
+        float x[8], y[8], cc[8], ss[8];
+        bool valid;
+        if (from_pool) {
+          if constexpr (!kPaged) {
+            const uint32_t* w = rk + i * 2 * Sh::WP;
+            valid = pk_seg[i] >= 0;
+            raw_to_f8<PoolT>(w, x);
+            raw_to_f8<PoolT>(w + Sh::WP, y);
+            if constexpr (SRC == SRC_POOL_I8) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) { x[e] *= pk_scale[i]; y[e] *= pk_scale[i]; }
+            }
+            if (valid) {
+              const int local = pk_seg[i] - p_seg0;
+              if (local >= 0 && local < NSEG) load_cs8(sCS + local * HALF + 8 * c, cc, ss);
+              else load_cs8(a.seg_cs + size_t(pk_seg[i]) * HALF + 8 * c, cc, ss);
+            }
+          } else {
+            valid = false;
+          }
+        } else {
+          const uint32_t* w = rk + i * 2 * Sh::WA;
+          valid = kk < nvalid;
+          raw_to_f8<T>(w, x);
+          raw_to_f8<T>(w + Sh::WA, y);
+          if (valid) load_cs8(a.suf_cs + (size_t(b) * S + k0 + kk) * HALF + 8 * c, cc, ss);
+        }
+        if (valid) {
+          rotate8(x, y, cc, ss);
+          store8(dst, x);
+          store8(dst + HALF, y);
+        } else {
+          store8_zero(dst);
+          store8_zero(dst + HALF);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < Sh::NVU; ++i) {
+        const int u = tid + i * NT;
+        if (u >= Sh::VU_TOT) continue;
+        const int c = u / KT;
+        float x[8];
+        if (from_pool) {
+          if constexpr (!kPaged) {
+            raw_to_f8<PoolT>(rv + i * Sh::WP, x);
+            if constexpr (SRC == SRC_POOL_I8) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) x[e] *= pv_scale;
+            }
+          }
+        } else {
+          raw_to_f8<T>(rv + i * Sh::WA, x);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sV[(8 * c + e) * L::LDV + kkv] = from_f<T>(x[e]);
+      }
+      (void)sizeof(RawT);
+    } else {
+      constexpr int EPV = Sh::EPV;
+#pragma unroll
+      for (int i = 0; i < Sh::NPK; ++i) {
+        const int u = tid + i * NT;
+        if (u >= Sh::PK_TOT) continue;
+        const int kk = u / (D / EPV), vec = u % (D / EPV);
+        *reinterpret_cast<uint4*>(sK + kk * L::LDK + vec * EPV) =
+            make_uint4(rk[4 * i], rk[4 * i + 1], rk[4 * i + 2], rk[4 * i + 3]);
+      }
+#pragma unroll
+      for (int i = 0; i < Sh::NPV; ++i) {
+        const int u = tid + i * NT;
+        if (u >= Sh::PV_TOT) continue;
+        const int d = u / (KT / EPV), vec = u % (KT / EPV);
+        uint4 val = make_uint4(rv[4 * i], rv[4 * i + 1], rv[4 * i + 2], rv[4 * i + 3]);
+        if (vec * EPV + EPV > nvalid) val = keep_first<T>(val, nvalid - vec * EPV);
+        *reinterpret_cast<uint4*>(sV + d * L::LDV + vec * EPV) = val;
+      }
+    }
+  };
 
   float m_run = kNegInf, l_run = 0.f;
   f32x16 o[NDB];
@@ -361,50 +662,32 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnParams a) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
 
-  for (int tile = it.tile0; tile < it.tile1; ++tile) {
+  const int t0 = it.tile0, t1 = it.tile1;
+  fetch_idx(t0);
+  fetch_data(t0);
+  if (t0 + 1 < t1) fetch_idx(t0 + 1);
+
+  for (int tile = t0; tile < t1; ++tile) {
     const bool suffix = tile >= nct;
     const int k0 = suffix ? (tile - nct) * KT : tile * KT;
     const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
 
-    __syncthreads();   // previous tile fully consumed
-    if (suffix) {
-      const T* ksb = static_cast<const T*>(a.k_suf);
-      const T* vsb = static_cast<const T*>(a.v_suf);
-      load_rows_tile<T, D, T>(sK, sV, nvalid,
-          [&](int kk, const T*& kp, const T*& vp, float& ks, float& vs, const float2*& cs) {
-            const size_t row = (size_t(b) * S + k0 + kk) * a.Hkv + g;
-            kp = ksb + row * D;
-            vp = vsb + row * D;
-            ks = vs = 1.f;
-            cs = a.suf_cs + (size_t(b) * S + k0 + kk) * (D / 2);
-          });
-    } else if constexpr (SRC == SRC_PAGED) {
-      const int page = a.block_table[size_t(b) * a.max_pages + k0 / a.PS];
-      const int off = k0 % a.PS;
-      const size_t ph = size_t(page) * a.Hkv + g;
-      const T* kpage = static_cast<const T*>(a.k) + (ph * a.PS + off) * D;
-      const T* vpage = static_cast<const T*>(a.v) + ph * D * a.PS + off;
-      load_paged_tile<T, D>(sK, sV, kpage, vpage, a.PS, nvalid);
-    } else {
-      const PoolT* kpool = static_cast<const PoolT*>(a.k);
-      const PoolT* vpool = static_cast<const PoolT*>(a.v);
-      load_rows_tile<T, D, PoolT>(sK, sV, nvalid,
-          [&](int kk, const PoolT*& kp, const PoolT*& vp, float& ks, float& vs,
-              const float2*& cs) {
-            const int slot = slot0 + k0 + kk;
-            const size_t row = size_t(a.slot_src[slot]) * a.Hkv + g;
-            kp = kpool + row * D;
-            vp = vpool + row * D;
-            if constexpr (SRC == SRC_POOL_I8) {
-              ks = a.k_scale[row];
-              vs = a.v_scale[row];
-            } else {
-              ks = vs = 1.f;
-            }
-            cs = a.seg_cs + size_t(a.slot_seg[slot]) * (D / 2);
-          });
+    if constexpr (!kPaged) {
+      // every read of the previous tile's cos/sin cache finished before the
+      // barrier that preceded the previous compute
+      if (!suffix) {
+#pragma unroll
+        for (int j = 0; j < Sh::NCS; ++j) {
+          const int e = tid + j * NT;
+          if (e < Sh::CS_TOT) sCS[e] = pcs[j];
+        }
+      }
     }
+    __syncthreads();   // previous tile consumed; cos/sin cache visible
+    commit(tile);
     __syncthreads();
+    if (tile + 1 < t1) fetch_data(tile + 1);
+    if (tile + 2 < t1) fetch_idx(tile + 2);
 
     // ---- S^T = K Q^T: two 32-key blocks, accumulator lane = query
     f32x16 s[2];
@@ -424,21 +707,24 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnParams a) {
 
     // ---- mask and online softmax (base 2); accumulator value v of block kb
     // holds key 32*kb + 8*(v/4) + 4*half + v%4 of the tile
+    if (suffix || nvalid < KT) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = kb * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+          const bool vis = key < nvalid && (!suffix || k0 + key <= t);
+          if (!vis) s[kb][v] = kNegInf;
+        }
+    }
     float mt = kNegInf;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = kb * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-        const bool vis = key < nvalid && (!suffix || k0 + key <= t);
-        const float x = vis ? s[kb][v] : kNegInf;
-        s[kb][v] = x;
-        mt = fmaxf(mt, x);
-      }
+      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s[kb][v]);
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float m_new = fmaxf(m_run, mt);
     const float m_ref = (m_new == kNegInf) ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
     float psum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -448,12 +734,16 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnParams a) {
         s[kb][v] = p;
         psum += p;
       }
-    l_run = l_run * alpha + psum;
+    if (__any(m_new > m_run)) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
+    }
+    l_run += psum;
     m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
 
     // ---- O^T += V^T P^T.  Chunk c takes accumulator values
     // v = KPL*(c % CPB) + e of block c / CPB; the matching key is read from sV.
@@ -479,8 +769,7 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnParams a) {
           const int kofs = 8 * (v0 >> 2);
           const uint2 lo = *reinterpret_cast<const uint2*>(vrow + kofs);
           const uint2 hi = *reinterpret_cast<const uint2*>(vrow + kofs + 8);
-          const uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
-          va = __builtin_bit_cast(Op, u);
+          va = __builtin_bit_cast(Op, make_uint4(lo.x, lo.y, hi.x, hi.y));
         }
         o[db] = M::run(va, pb, o[db]);
       }
@@ -489,85 +778,75 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnParams a) {
 
   // ---- epilogue: accumulator value v of block db holds d = 32*db + 8*(v/4) + 4*half + v%4
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (!row_ok) return;
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float lse_val = l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2 : kNegInf;
-  if (it.partial < 0) {
-    T* orow = static_cast<T*>(a.out) + ((size_t(b) * S + t) * a.Hq + h) * D;
+  if (row_ok) {
+    if (it.partial < 0) {
+      T* orow = static_cast<T*>(a.out) + ((size_t(b) * S + t) * a.Hq + h) * D;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+      for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d = 32 * db + 8 * i + 4 * half;
-        if constexpr (sizeof(T) == 4) {
-          *reinterpret_cast<float4*>(orow + d) =
-              make_float4(o[db][4 * i] * inv, o[db][4 * i + 1] * inv, o[db][4 * i + 2] * inv,
-                          o[db][4 * i + 3] * inv);
-        } else {
-          uint2 u;
-          u.x = pack_bf16(o[db][4 * i] * inv, o[db][4 * i + 1] * inv);
-          u.y = pack_bf16(o[db][4 * i + 2] * inv, o[db][4 * i + 3] * inv);
-          *reinterpret_cast<uint2*>(orow + d) = u;
+        for (int i = 0; i < 4; ++i) {
+          const int d = 32 * db + 8 * i + 4 * half;
+          if constexpr (sizeof(T) == 4) {
+            *reinterpret_cast<float4*>(orow + d) =
+                make_float4(o[db][4 * i] * inv, o[db][4 * i + 1] * inv,
+                            o[db][4 * i + 2] * inv, o[db][4 * i + 3] * inv);
+          } else {
+            uint2 u;
+            u.x = pack_bf16(o[db][4 * i] * inv, o[db][4 * i + 1] * inv);
+            u.y = pack_bf16(o[db][4 * i + 2] * inv, o[db][4 * i + 3] * inv);
+            *reinterpret_cast<uint2*>(orow + d) = u;
+          }
         }
-      }
-    if (a.lse && half == 0) a.lse[(size_t(b) * a.Hq + h) * S + t] = lse_val;
-  } else {
-    float* prow = a.part_o + (size_t(it.partial) * a.RB + rloc) * D;
+      if (a.lse && half == 0) a.lse[(size_t(b) * a.Hq + h) * S + t] = lse_val;
+    } else {
+      float* prow = a.part_o + (size_t(it.partial) * a.RB + rloc) * D;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+      for (int db = 0; db < NDB; ++db)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d = 32 * db + 8 * i + 4 * half;
-        *reinterpret_cast<float4*>(prow + d) =
-            make_float4(o[db][4 * i] * inv, o[db][4 * i + 1] * inv, o[db][4 * i + 2] * inv,
-                        o[db][4 * i + 3] * inv);
-      }
-    if (half == 0) a.part_lse[size_t(it.partial) * a.RB + rloc] = lse_val;
+        for (int i = 0; i < 4; ++i) {
+          const int d = 32 * db + 8 * i + 4 * half;
+          *reinterpret_cast<float4*>(prow + d) =
+              make_float4(o[db][4 * i] * inv, o[db][4 * i + 1] * inv,
+                          o[db][4 * i + 2] * inv, o[db][4 * i + 3] * inv);
+        }
+      if (half == 0) a.part_lse[size_t(it.partial) * a.RB + rloc] = lse_val;
+    }
+  }
+
+  // ---- the last split of a row block to finish combines all of its splits
+  if (it.merge >= 0 && a.merge_in_kernel) {
+    __threadfence();                       // release this split's partial (agent scope)
+    __syncthreads();
+    if (tid == 0) {
+      const int old = atomicAdd(a.counters + it.merge, 1);
+      s_last = (old == a.merges[it.merge].nsplit - 1) ? 1 : 0;
+    }
+    __syncthreads();
+    if (s_last) {
+      __threadfence();                     // acquire the other splits' partials
+      const MergeGroup mg = a.merges[it.merge];
+      merge_rows<T, D>(mg, 0, mg.nrows, a.part_o, a.part_lse, a.RB, a.Hq, G, S, a.out, a.lse,
+                       tid, NT);
+      if (tid == 0) a.counters[it.merge] = 0;   // ready for the next launch
+    }
   }
 }
 
 // ----------------------------------------------------------------------------
-// merge of key splits
+// merge of key splits as its own kernel (row blocks with many splits)
 // ----------------------------------------------------------------------------
 
 template <typename T, int D>
 __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
-  constexpr int TPR = D / 4;                  // threads per row, 4 elements each
-  constexpr int RPW = 256 / TPR;              // rows per workgroup
+  constexpr int RPW = 256 / (D / 4);          // rows per workgroup
   const MergeGroup mg = a.groups[blockIdx.x];
-  const int rloc = blockIdx.y * RPW + threadIdx.x / TPR;
-  if (rloc >= mg.nrows) return;
-  const int d = 4 * (threadIdx.x % TPR);
-  float mx = kNegInf;
-  for (int i = 0; i < mg.nsplit; ++i)
-    mx = fmaxf(mx, a.part_lse[size_t(mg.part0 + i) * a.RB + rloc]);
-  float z = 0.f;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int i = 0; i < mg.nsplit; ++i) {
-    const float li = a.part_lse[size_t(mg.part0 + i) * a.RB + rloc];
-    const float w = (li == kNegInf) ? 0.f : __expf(li - mx);
-    z += w;
-    if (w != 0.f) {
-      const float4 v = *reinterpret_cast<const float4*>(
-          a.part_o + (size_t(mg.part0 + i) * a.RB + rloc) * D + d);
-      acc.x += w * v.x; acc.y += w * v.y; acc.z += w * v.z; acc.w += w * v.w;
-    }
-  }
-  const float inv = z > 0.f ? 1.f / z : 0.f;
-  const int r = mg.row0 + rloc;
-  const int t = r / a.G, h = mg.g * a.G + r % a.G;
-  T* orow = static_cast<T*>(a.out) + ((size_t(mg.b) * a.S + t) * a.Hq + h) * D;
-  if constexpr (sizeof(T) == 4) {
-    *reinterpret_cast<float4*>(orow + d) =
-        make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
-  } else {
-    uint2 u;
-    u.x = pack_bf16(acc.x * inv, acc.y * inv);
-    u.y = pack_bf16(acc.z * inv, acc.w * inv);
-    *reinterpret_cast<uint2*>(orow + d) = u;
-  }
-  if (a.lse && d == 0)
-    a.lse[(size_t(mg.b) * a.Hq + h) * a.S + t] = z > 0.f ? mx + __logf(z) : kNegInf;
+  const int rlo = blockIdx.y * RPW;
+  const int rhi = min(rlo + RPW, mg.nrows);
+  if (rlo >= rhi) return;
+  merge_rows<T, D>(mg, rlo, rhi, a.part_o, a.part_lse, a.RB, a.Hq, a.G, a.S, a.out, a.lse,
+                   threadIdx.x, 256);
 }
 
 // ----------------------------------------------------------------------------
@@ -599,8 +878,8 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
     T* dst = kpage + size_t(kk) * D + 8 * c;
     if (kk < nvalid) {
       const int slot = slot0 + k0 + kk;
-      const int src = a.slot_src[slot];
-      const size_t row = size_t(src) * a.Hkv + g;
+      const int2 si = a.slot_info[slot];
+      const size_t row = size_t(si.x) * a.Hkv + g;
       float x[8], y[8], cc[8], ss[8];
       load8(kpool + row * D + 8 * c, x);
       load8(kpool + row * D + 8 * c + D / 2, y);
@@ -609,12 +888,12 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) { x[e] *= ks; y[e] *= ks; }
       }
-      load_cs8(a.seg_cs + size_t(a.slot_seg[slot]) * (D / 2) + 8 * c, cc, ss);
+      load_cs8(a.seg_cs + size_t(si.y) * (D / 2) + 8 * c, cc, ss);
       rotate8(x, y, cc, ss);
       store8(dst, x);
       store8(dst + D / 2, y);
       if (g == 0 && c == 0) {
-        if (a.out_src_row) a.out_src_row[slot] = src;
+        if (a.out_src_row) a.out_src_row[slot] = si.x;
         if (a.out_pos) a.out_pos[slot] = a.slot_pos[slot];
       }
     } else {
@@ -628,7 +907,7 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
     const int c = u / KT, kk = u % KT;
     float x[8];
     if (kk < nvalid) {
-      const size_t row = size_t(a.slot_src[slot0 + k0 + kk]) * a.Hkv + g;
+      const size_t row = size_t(a.slot_info[slot0 + k0 + kk].x) * a.Hkv + g;
       load8(vpool + row * D + 8 * c, x);
       if constexpr (sizeof(PoolT) == 1) {
         const float vs = a.v_scale[row];
@@ -669,7 +948,10 @@ T* at_mut(void* base, size_t off) {
 
 template <typename T, int D, int SRC>
 hipError_t launch_attn_t(const AttnParams& ap, int n_items, int threads, hipStream_t st) {
-  hipLaunchKernelGGL((attn_kernel<T, D, SRC>), dim3(n_items), dim3(threads), 0, st, ap);
+  if (threads == 512)
+    hipLaunchKernelGGL((attn_kernel<T, D, SRC, 512>), dim3(n_items), dim3(512), 0, st, ap);
+  else
+    hipLaunchKernelGGL((attn_kernel<T, D, SRC, 256>), dim3(n_items), dim3(256), 0, st, ap);
   return hipGetLastError();
 }
 
@@ -685,7 +967,7 @@ hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const vo
                             const float* k_scale, const float* v_scale, const void* q,
                             const void* k_suf, const void* v_suf, void* out, float* lse,
                             hipStream_t st) {
-  const void* ws = p.d_workspace;
+  void* ws = p.d_workspace;
   AttnParams ap{};
   ap.Hq = p.cfg.n_q_heads;
   ap.Hkv = p.cfg.n_kv_heads;
@@ -694,14 +976,17 @@ hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const vo
   ap.PS = p.page_size;
   ap.max_pages = p.max_pages;
   ap.RB = p.rows_per_block;
+  ap.n_seg = p.n_segments;
+  ap.merge_in_kernel = p.merge_in_kernel ? 1 : 0;
   ap.qscale = p.qscale_log2;
   ap.req_slot0 = at<int>(ws, p.ws.req_slot0);
-  ap.slot_src = at<int>(ws, p.ws.slot_src);
-  ap.slot_seg = at<int>(ws, p.ws.slot_seg);
+  ap.slot_info = at<int2>(ws, p.ws.slot_info);
   ap.seg_cs = at<float2>(ws, p.ws.seg_cs);
   ap.suf_cs = at<float2>(ws, p.ws.suf_cs);
   ap.block_table = at<int>(ws, p.ws.block_table);
   ap.items = at<WorkItem>(ws, p.ws.items);
+  ap.merges = at<MergeGroup>(ws, p.ws.merges);
+  ap.counters = at_mut<int>(ws, p.ws.counters);
   ap.k = k;
   ap.v = v;
   ap.k_scale = k_scale;
@@ -711,8 +996,8 @@ hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const vo
   ap.v_suf = v_suf;
   ap.out = out;
   ap.lse = lse;
-  ap.part_o = at_mut<float>(p.d_workspace, p.ws.part_o);
-  ap.part_lse = at_mut<float>(p.d_workspace, p.ws.part_lse);
+  ap.part_o = at_mut<float>(ws, p.ws.part_o);
+  ap.part_lse = at_mut<float>(ws, p.ws.part_lse);
   const int n = static_cast<int>(p.items.size());
   const int threads = 64 * (p.rows_per_block / kRowsPerWave);
   const int D = p.cfg.head_dim;
@@ -726,7 +1011,7 @@ hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const vo
 }
 
 hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st) {
-  if (p.merges.empty()) return hipSuccess;
+  if (p.merges.empty() || p.merge_in_kernel) return hipSuccess;
   MergeParams mp{};
   mp.Hq = p.cfg.n_q_heads;
   mp.G = p.group;
@@ -761,8 +1046,7 @@ hipError_t launch_compose(const Plan& p, int pool_dtype, const void* k, const vo
   cp.PS = p.page_size;
   cp.max_pages = p.max_pages;
   cp.req_slot0 = at<int>(p.d_workspace, p.ws.req_slot0);
-  cp.slot_src = at<int>(p.d_workspace, p.ws.slot_src);
-  cp.slot_seg = at<int>(p.d_workspace, p.ws.slot_seg);
+  cp.slot_info = at<int2>(p.d_workspace, p.ws.slot_info);
   cp.slot_pos = at<int>(p.d_workspace, p.ws.slot_pos);
   cp.seg_cs = at<float2>(p.d_workspace, p.ws.seg_cs);
   cp.block_table = at<int>(p.d_workspace, p.ws.block_table);

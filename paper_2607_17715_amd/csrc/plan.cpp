@@ -78,13 +78,16 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
     err = fmt("page_size must be a positive multiple of ", kKeyTile, ", got ", o.page_size);
     return C2KV_E_INVAL;
   }
-  if (o.rows_per_block != 0 && o.rows_per_block != 32 && o.rows_per_block != 64 &&
-      o.rows_per_block != 128 && o.rows_per_block != 256) {
-    err = fmt("rows_per_block must be 0, 32, 64, 128 or 256, got ", o.rows_per_block);
+  if (o.rows_per_block != 0 && o.rows_per_block != 128 && o.rows_per_block != 256) {
+    err = fmt("rows_per_block must be 0, 128 or 256, got ", o.rows_per_block);
     return C2KV_E_INVAL;
   }
   if (o.kv_splits < 0 || o.num_cus < 0) {
     err = "kv_splits and num_cus must be >= 0";
+    return C2KV_E_INVAL;
+  }
+  if (o.merge_mode < 0 || o.merge_mode > 2) {
+    err = fmt("merge_mode must be 0, 1 or 2, got ", o.merge_mode);
     return C2KV_E_INVAL;
   }
   if (o.num_cus == 0) o.num_cus = 256;
@@ -215,12 +218,9 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   const int64_t G = p.group, S = suffix_len;
   const int64_t R = G * S;            // query rows per (request, kv-head)
   int RB = o.rows_per_block;
-  if (RB == 0) {
-    RB = 32;
-    while (RB < R && RB < 256) RB *= 2;
-  }
+  if (RB == 0) RB = R >= 256 ? 256 : 128;
   p.rows_per_block = RB;
-  const int wgs_per_cu = RB >= 256 ? 1 : (RB == 128 ? 2 : 4);
+  const int wgs_per_cu = RB >= 256 ? 1 : 2;
   const int64_t target = int64_t(o.num_cus) * wgs_per_cu;
   const int32_t n_rb = ceil_div(R, RB);
   struct Group { int32_t b, g, row0, nrows, tiles; };
@@ -240,26 +240,62 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       }
   }
   const int64_t per_item = std::max<int64_t>(2, (total_tiles + target - 1) / target);
+  std::vector<WorkItem> items;
   for (const Group& gr : groups) {
     int32_t ns = o.kv_splits > 0 ? o.kv_splits : ceil_div(gr.tiles, per_item);
     ns = std::max(1, std::min(ns, gr.tiles));
     p.max_splits = std::max(p.max_splits, ns);
-    int32_t part0 = -1;
+    int32_t part0 = -1, merge = -1;
     if (ns > 1) {
       part0 = p.n_partials;
+      merge = static_cast<int32_t>(p.merges.size());
       p.merges.push_back({gr.b, gr.g, gr.row0, gr.nrows, part0, ns, 0, 0});
       p.n_partials += ns;
     }
     for (int s = 0; s < ns; ++s) {
       const int32_t t0 = static_cast<int32_t>(int64_t(gr.tiles) * s / ns);
       const int32_t t1 = static_cast<int32_t>(int64_t(gr.tiles) * (s + 1) / ns);
-      p.items.push_back({gr.b, gr.g, gr.row0, gr.nrows, t0, t1, ns > 1 ? part0 + s : -1, 0});
+      items.push_back({gr.b, gr.g, gr.row0, gr.nrows, t0, t1, ns > 1 ? part0 + s : -1, merge});
     }
   }
-  // heaviest items first, so the ragged tail of the grid is short
-  std::stable_sort(p.items.begin(), p.items.end(), [](const WorkItem& a, const WorkItem& b) {
-    return (a.tile1 - a.tile0) > (b.tile1 - b.tile0);
-  });
+  p.merge_in_kernel = o.merge_mode == 1 || (o.merge_mode == 0 && p.max_splits <= 8);
+
+  // XCD-aware order.  Workgroups are dealt to the 8 XCDs round-robin by index,
+  // and each XCD has its own L2.  Items of one (request, kv-head) read the same
+  // keys, values and queries, so they are kept on one XCD: (b, g) pairs go to the
+  // least-loaded XCD queue, queues hold their heaviest items first, and the
+  // grid interleaves the queues.
+  constexpr int kXcds = 8;
+  std::vector<std::vector<WorkItem>> queue(kXcds);
+  std::vector<int64_t> load(kXcds, 0);
+  {
+    std::vector<std::pair<int64_t, int64_t>> pairs;   // (-tiles, b * H + g)
+    std::vector<int64_t> tiles_of(size_t(B) * cfg.n_kv_heads, 0);
+    for (const WorkItem& w : items) tiles_of[size_t(w.b) * cfg.n_kv_heads + w.g] += w.tile1 - w.tile0;
+    for (size_t k = 0; k < tiles_of.size(); ++k) pairs.push_back({-tiles_of[k], int64_t(k)});
+    std::sort(pairs.begin(), pairs.end());
+    std::vector<int> bin_of(tiles_of.size(), 0);
+    for (const auto& pr : pairs) {
+      const int x = static_cast<int>(std::min_element(load.begin(), load.end()) - load.begin());
+      bin_of[pr.second] = x;
+      load[x] += -pr.first;
+    }
+    for (const WorkItem& w : items) queue[bin_of[size_t(w.b) * cfg.n_kv_heads + w.g]].push_back(w);
+    for (auto& q : queue)
+      std::stable_sort(q.begin(), q.end(), [](const WorkItem& a, const WorkItem& b) {
+        return (a.tile1 - a.tile0) > (b.tile1 - b.tile0);
+      });
+  }
+  std::vector<size_t> head(kXcds, 0);
+  for (size_t n = 0; n < items.size(); ++n) {
+    int x = static_cast<int>(n % kXcds);
+    if (head[x] >= queue[x].size()) {           // this queue ran dry: take the fullest one
+      size_t best = 0;
+      for (int y = 0; y < kXcds; ++y)
+        if (queue[y].size() - head[y] > best) { best = queue[y].size() - head[y]; x = y; }
+    }
+    p.items.push_back(queue[x][head[x]++]);
+  }
 
   // ---- workspace image --------------------------------------------------------
   const int D = cfg.head_dim, H = D / 2;
@@ -268,8 +304,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t at = off; off = align256(off + std::max<size_t>(bytes, 4)); return at; };
   w.req_slot0 = take(sizeof(int32_t) * (B + 1));
-  w.slot_src = take(sizeof(int32_t) * total);
-  w.slot_seg = take(sizeof(int32_t) * total);
+  w.slot_info = take(sizeof(int32_t) * 2 * total);
   w.slot_pos = take(sizeof(int32_t) * total);
   w.seg_cs = take(sizeof(float) * 2 * size_t(std::max(nseg, 1)) * H);
   w.suf_cs = take(sizeof(float) * 2 * size_t(B) * S * H);
@@ -277,6 +312,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   w.compose_tiles = take(sizeof(int32_t) * p.compose_tiles.size());
   w.items = take(sizeof(WorkItem) * p.items.size());
   w.merges = take(sizeof(MergeGroup) * p.merges.size());
+  w.counters = take(sizeof(int32_t) * p.merges.size());
   w.table_bytes = off;
   w.part_o = take(sizeof(float) * size_t(p.n_partials) * RB * D);
   w.part_lse = take(sizeof(float) * size_t(p.n_partials) * RB);
@@ -287,8 +323,13 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
     if (bytes) std::memcpy(p.image.data() + at, src, bytes);
   };
   put(w.req_slot0, p.req_slot0.data(), sizeof(int32_t) * (B + 1));
-  put(w.slot_src, p.slot_src.data(), sizeof(int32_t) * total);
-  put(w.slot_seg, p.slot_seg.data(), sizeof(int32_t) * total);
+  {
+    int32_t* si = reinterpret_cast<int32_t*>(p.image.data() + w.slot_info);
+    for (int64_t i = 0; i < total; ++i) {
+      si[2 * i] = p.slot_src[i];
+      si[2 * i + 1] = p.slot_seg[i];
+    }
+  }
   put(w.slot_pos, p.slot_pos.data(), sizeof(int32_t) * total);
   put(w.block_table, p.block_table.data(), sizeof(int32_t) * p.block_table.size());
   put(w.compose_tiles, p.compose_tiles.data(), sizeof(int32_t) * p.compose_tiles.size());

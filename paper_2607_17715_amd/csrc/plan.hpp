@@ -19,9 +19,10 @@ constexpr int kRowsPerWave = 32;    // query rows one wavefront owns (MFMA 32-wi
 // One attention workgroup: query rows [row0, row0 + nrows) of (request b,
 // kv-head g) in t-major order (row r = t * G + head-within-group), over key
 // tiles [tile0, tile1) of the combined tile list (cached tiles first, then the
-// suffix tiles this row block can see).  partial < 0: write the final output.
+// suffix tiles this row block can see).  partial < 0: write the final output;
+// otherwise write partial `partial` of merge group `merge`.
 struct WorkItem {
-  int32_t b, g, row0, nrows, tile0, tile1, partial, pad;
+  int32_t b, g, row0, nrows, tile0, tile1, partial, merge;
 };
 
 // Row block whose key splits are combined by the merge kernel.
@@ -32,8 +33,7 @@ struct MergeGroup {
 // Byte offsets of the device tables inside the workspace.
 struct WorkspaceLayout {
   size_t req_slot0 = 0;   // int32 [B+1]
-  size_t slot_src = 0;    // int32 [total_slots]
-  size_t slot_seg = 0;    // int32 [total_slots]
+  size_t slot_info = 0;   // int32x2 [total_slots] (pool row, segment)
   size_t slot_pos = 0;    // int32 [total_slots]
   size_t seg_cs = 0;      // float2 [n_seg][D/2]   cos/sin(delta * theta_i)
   size_t suf_cs = 0;      // float2 [B][S][D/2]    cos/sin((span_end + t) * theta_i)
@@ -41,6 +41,7 @@ struct WorkspaceLayout {
   size_t compose_tiles = 0; // int32x2 [n_compose_tiles] (b, tile)
   size_t items = 0;       // WorkItem [n_items]
   size_t merges = 0;      // MergeGroup [n_merge]
+  size_t counters = 0;    // int32 [n_merge], zero between launches
   size_t table_bytes = 0; // end of the tables (uploaded image size)
   size_t part_o = 0;      // float [n_partials][rows_per_block][D]
   size_t part_lse = 0;    // float [n_partials][rows_per_block]
@@ -74,6 +75,7 @@ struct Plan {
   std::vector<WorkItem> items;
   std::vector<MergeGroup> merges;
   int32_t n_partials = 0, max_splits = 1;
+  bool merge_in_kernel = false;   // last split of a row block merges (else a merge kernel)
 
   // tables in float (host image)
   WorkspaceLayout ws;

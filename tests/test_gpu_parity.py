@@ -131,8 +131,11 @@ def test_compose_delta0_is_a_bit_exact_copy():
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("opts", [dict(kv_splits=1), dict(kv_splits=2), dict(kv_splits=7),
-                                  dict(rows_per_block=32), dict(rows_per_block=64),
-                                  dict(rows_per_block=256, kv_splits=3),
+                                  dict(kv_splits=3, merge_mode=1),
+                                  dict(kv_splits=3, merge_mode=2),
+                                  dict(kv_splits=12, merge_mode=1),
+                                  dict(rows_per_block=128), dict(rows_per_block=256),
+                                  dict(rows_per_block=256, kv_splits=3, merge_mode=2),
                                   dict(page_size=256)])
 def test_launch_shape_invariance(opts):
     w = synth.small(batch=2, n_q_heads=16, n_kv_heads=4, suffix_len=45,
