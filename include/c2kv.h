@@ -195,11 +195,12 @@ c2kv_status c2kv_compose_attend(const c2kv_plan* plan, const c2kv_pool* pool,
                                 const void* q, const void* k_suf, const void* v_suf,
                                 void* out, float* lse, void* stream);
 
-/* Per-kernel timing for measurement: when enabled, every kernel launch is
- * bracketed by HIP events on its own stream.  c2kv_timing_read synchronises on
- * the recorded events and returns the summed milliseconds and launch count of
- * kernel `name` ("compose", "attn_paged", "attn_pool", "merge") since the last
- * reset.  Timing adds event records between launches; leave it off otherwise. */
+/* Per-kernel timing for measurement: when enabled, every kernel is launched
+ * with a pair of HIP events that its dispatch stamps at kernel start and end
+ * (on the kernel's own stream).  c2kv_timing_read synchronises on them and
+ * returns the summed milliseconds and launch count of kernel `name`
+ * ("compose", "attn_paged", "attn_pool", "merge") since the last reset.
+ * Launches with timing on are not meant for graph capture. */
 c2kv_status c2kv_timing_enable(int32_t on);
 c2kv_status c2kv_timing_reset(void);
 c2kv_status c2kv_timing_read(const char* name, double* total_ms, int64_t* launches);

@@ -50,15 +50,16 @@ hipEvent_t take_event() {
   return e;
 }
 
-// Runs `launch` on `st`; when timing is on, brackets it with events filed under `name`.
+// Runs `launch(ev0, ev1)`; when timing is on, the events (stamped by the
+// kernel's own dispatch at its start and end) are filed under `name`.
 template <typename F>
-hipError_t timed(const char* name, hipStream_t st, F&& launch) {
+hipError_t timed(const char* name, F&& launch) {
   bool on;
   {
     std::lock_guard<std::mutex> lk(g_timing.mu);
     on = g_timing.on;
   }
-  if (!on) return launch();
+  if (!on) return launch(nullptr, nullptr);
   hipEvent_t a, b;
   {
     std::lock_guard<std::mutex> lk(g_timing.mu);
@@ -66,11 +67,7 @@ hipError_t timed(const char* name, hipStream_t st, F&& launch) {
     b = take_event();
   }
   if (!a || !b) return hipErrorOutOfMemory;
-  hipError_t e = hipEventRecord(a, st);
-  if (e != hipSuccess) return e;
-  e = launch();
-  if (e != hipSuccess) return e;
-  e = hipEventRecord(b, st);
+  hipError_t e = launch(a, b);
   if (e != hipSuccess) return e;
   std::lock_guard<std::mutex> lk(g_timing.mu);
   g_timing.recs[name].push_back({a, b});
@@ -234,9 +231,9 @@ c2kv_status c2kv_compose(const c2kv_plan* plan, const c2kv_pool* pool, void* k_p
   if ((!k_pages || !v_pages) && p.n_pages > 0)
     return fail(C2KV_E_INVAL, "k_pages and v_pages must not be NULL");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = timed("compose", s, [&] {
+  hipError_t e = timed("compose", [&](hipEvent_t e0, hipEvent_t e1) {
     return c2kv::launch_compose(p, pool->dtype, pool->k, pool->v, pool->k_scale, pool->v_scale,
-                                k_pages, v_pages, slot_src_row, slot_pos, s);
+                                k_pages, v_pages, slot_src_row, slot_pos, s, e0, e1);
   });
   if (e != hipSuccess) return hip_fail(e, "compose launch");
   if (block_table) {
@@ -253,12 +250,15 @@ static c2kv_status run_attention(const c2kv::Plan& p, int src_kind, const char* 
                                  const float* vs, const void* q, const void* k_suf,
                                  const void* v_suf, void* out, float* lse, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  hipError_t e = timed(name, s, [&] {
-    return c2kv::launch_attention(p, src_kind, k, v, ks, vs, q, k_suf, v_suf, out, lse, s);
+  hipError_t e = timed(name, [&](hipEvent_t e0, hipEvent_t e1) {
+    return c2kv::launch_attention(p, src_kind, k, v, ks, vs, q, k_suf, v_suf, out, lse, s, e0,
+                                  e1);
   });
   if (e != hipSuccess) return hip_fail(e, "attention launch");
-  if (!p.merges.empty()) {
-    e = timed("merge", s, [&] { return c2kv::launch_merge(p, out, lse, s); });
+  if (!p.merges.empty() && !p.merge_in_kernel) {
+    e = timed("merge", [&](hipEvent_t e0, hipEvent_t e1) {
+      return c2kv::launch_merge(p, out, lse, s, e0, e1);
+    });
     if (e != hipSuccess) return hip_fail(e, "merge launch");
   }
   return C2KV_OK;

@@ -257,33 +257,32 @@ struct MergeParams {
 
 template <typename T, int D>
 struct Lds {
-  static constexpr int PAD = 16 / sizeof(T);
-  static constexpr int LDK = D + PAD;       // sK[KT][LDK]: keys at final positions
-  static constexpr int LDV = KT + PAD;      // sV[D][LDV]: values transposed
+  // keys: rows of D elements padded by 16 bytes (16-byte reads, 4-bank row shift);
+  // transposed values: rows of KT keys padded by 8 bytes, so that 32 consecutive
+  // rows map 8-byte reads onto distinct bank pairs
+  static constexpr int LDK = D + 16 / int(sizeof(T));
+  static constexpr int LDV = KT + 8 / int(sizeof(T));
+  static constexpr int TILE = KT * LDK + D * LDV;   // elements of one stage
 };
-
-constexpr int NSEG = 4;   // segments whose cos/sin a key tile caches in LDS
 
 constexpr int imax(int a, int b) { return a > b ? a : b; }
 
 // Per-thread work of one key tile for an NT-thread workgroup.
 template <typename T, typename PoolT, int D, int NT, bool PAGED>
 struct Shape {
-  static constexpr int KU_TOT = KT * (D / 16);   // key units: (chunk, chunk + D/2) pairs
-  static constexpr int VU_TOT = KT * (D / 8);    // value units: 8-element chunks
+  static constexpr int KU_TOT = KT * (D / 16);     // key units: (chunk, chunk + D/2) pairs
+  static constexpr int VU_TOT = (KT / 2) * (D / 8);// value units: 8-element chunk of 2 keys
   static constexpr int NKU = (KU_TOT + NT - 1) / NT;
   static constexpr int NVU = (VU_TOT + NT - 1) / NT;
-  static constexpr int EPV = 16 / sizeof(T);     // elements per 16-byte vector
-  static constexpr int PK_TOT = KT * D / EPV;    // page vectors, keys
-  static constexpr int PV_TOT = D * KT / EPV;    // page vectors, transposed values
+  static constexpr int EPV = 16 / sizeof(T);       // elements per 16-byte vector
+  static constexpr int PK_TOT = KT * D / EPV;      // page vectors, keys
+  static constexpr int PV_TOT = D * KT / EPV;      // page vectors, transposed values
   static constexpr int NPK = (PK_TOT + NT - 1) / NT;
   static constexpr int NPV = (PV_TOT + NT - 1) / NT;
-  static constexpr int WP = 2 * int(sizeof(PoolT));  // words per 8 pool elements
-  static constexpr int WA = 2 * int(sizeof(T));      // words per 8 act elements
+  static constexpr int WP = 2 * int(sizeof(PoolT));    // words per 8 pool elements
+  static constexpr int WA = 2 * int(sizeof(T));        // words per 8 act elements
   static constexpr int RKW = imax(NKU * 2 * WA, PAGED ? NPK * 4 : NKU * 2 * WP);
-  static constexpr int RVW = imax(NVU * WA, PAGED ? NPV * 4 : NVU * WP);
-  static constexpr int CS_TOT = NSEG * (D / 2);
-  static constexpr int NCS = (CS_TOT + NT - 1) / NT;
+  static constexpr int RVW = imax(NVU * 2 * WA, PAGED ? NPV * 4 : NVU * 2 * WP);
 };
 
 // ----------------------------------------------------------------------------
@@ -334,8 +333,15 @@ __device__ inline void merge_rows(const MergeGroup& mg, int rlo, int rhi, const 
 // attention
 // ----------------------------------------------------------------------------
 
-template <typename T, int D, int SRC, int NT>
-__global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
+// One workgroup = 8 wavefronts.  With KG = 1 each wavefront owns 32 query rows
+// (256 per workgroup) and every key of a tile; with KG = 2 four row groups of
+// 32 rows (128 per workgroup) each see one half of every 64-key tile, keep their
+// own online softmax, and the two halves are combined through LDS at the end.
+template <typename T, int D, int SRC, int KG>
+__global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
+  constexpr int NT = 512;
+  constexpr int NRG = 8 / KG;               // row groups
+  constexpr int NKB = 2 / KG;               // 32-key blocks per wavefront and tile
   using M = Mma<T>;
   using Op = typename M::Op;
   using L = Lds<T, D>;
@@ -351,9 +357,8 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   constexpr int HALF = D / 2;
   constexpr int KUPK = D / 16;              // key units per key
 
-  __shared__ __attribute__((aligned(16))) T sK[KT * L::LDK];
-  __shared__ __attribute__((aligned(16))) T sV[D * L::LDV];
-  __shared__ __attribute__((aligned(16))) float2 sCS[kPaged ? 2 : Sh::CS_TOT];
+  // two stages of [keys | transposed values]
+  __shared__ __attribute__((aligned(16))) T sbuf[2 * L::TILE];
   __shared__ int s_last;
 
   const int tid = threadIdx.x;
@@ -362,89 +367,42 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   const int qi = lane & 31, half = lane >> 5;
   const int b = it.b, g = it.g;
   const int S = a.S, G = a.G;
-  const int slot0 = a.req_slot0[b];
-  const int N = a.req_slot0[b + 1] - slot0;
+  const int slot0 = it.slot0;
+  const int N = it.nslots;
   const int nct = (N + KT - 1) / KT;
 
-  const int rloc = wave * 32 + qi;
+  const int rgrp = wave % NRG, kh = wave / NRG;
+  const int rloc = rgrp * 32 + qi;
   const bool row_ok = rloc < it.nrows;
   const int r = it.row0 + rloc;
   const int t = row_ok ? r / G : 0;
   const int h = g * G + (row_ok ? r % G : 0);
 
-  // ---- Q operand: RoPE at span_end + t, softmax scale and log2(e) folded in.
-  // Lane (qi, half) holds d = c*KSTEP + half*KPL + e in qop[c][e]; the RoPE
-  // partner d + D/2 sits in chunk c + NQC/2 of the same lane.
-  Op qop[NQC];
-  {
-    const T* qrow = static_cast<const T*>(a.q) + ((size_t(b) * S + t) * a.Hq + h) * D;
-    const float2* cs = a.suf_cs + (size_t(b) * S + t) * HALF;
-#pragma unroll
-    for (int c = 0; c < NQC / 2; ++c) {
-      const int d0 = c * KSTEP + half * KPL;
-      float x[KPL], y[KPL], cc[KPL], ss[KPL];
-      if (row_ok) {
-        if constexpr (KPL == 8) {
-          uint32_t wx[4], wy[4];
-          raw_load8<T>(wx, qrow + d0);
-          raw_load8<T>(wy, qrow + d0 + HALF);
-          float fx[8], fy[8];
-          raw_to_f8<T>(wx, fx);
-          raw_to_f8<T>(wy, fy);
-          float c8[8], s8[8];
-          load_cs8(cs + d0, c8, s8);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) { x[e] = fx[e]; y[e] = fy[e]; cc[e] = c8[e]; ss[e] = s8[e]; }
-        } else {
-          x[0] = to_f(qrow[d0]);
-          y[0] = to_f(qrow[d0 + HALF]);
-          const float2 w = cs[d0];
-          cc[0] = w.x;
-          ss[0] = w.y;
-        }
-#pragma unroll
-        for (int e = 0; e < KPL; ++e) {
-          rotate_pair(x[e], y[e], cc[e], ss[e]);
-          x[e] *= a.qscale;
-          y[e] *= a.qscale;
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < KPL; ++e) { x[e] = 0.f; y[e] = 0.f; }
-      }
-      if constexpr (KPL == 1) {
-        qop[c] = x[0];
-        qop[c + NQC / 2] = y[0];
-      } else {
-#pragma unroll
-        for (int e = 0; e < KPL; ++e) {
-          qop[c][e] = from_f<T>(x[e]);
-          qop[c + NQC / 2][e] = from_f<T>(y[e]);
-        }
-      }
-    }
-  }
-
-  // ---- tile pipeline: indices two tiles ahead, data one tile ahead --------
+  // ---- tile pipeline state: indices two tiles ahead, data one tile ahead ----
   uint32_t rk[Sh::RKW], rv[Sh::RVW];
-  int2 nk[Sh::NKU];
-  int2 nv = make_int2(-1, -1);
-  int n_seg0 = 0, n_page = 0;
-  int pk_seg[Sh::NKU];
-  float pk_scale[Sh::NKU];
-  float pv_scale = 1.f;
-  float2 pcs[Sh::NCS];
-  int p_seg0 = 0;
+  float ck[Sh::NKU][8], sk[Sh::NKU][8];     // cos/sin of this thread's key units
+  int cs_seg[Sh::NKU];                      // segment the pool cos/sin belong to
+  int2 nk[Sh::NKU], nv[2];                  // (row, segment) of the next tile's keys
+  int n_page = 0;
+  bool k_ok[Sh::NKU];
+  bool v_ok[2];
+  float k_scale[Sh::NKU], v_scale[2];
 #pragma unroll
-  for (int i = 0; i < Sh::NKU; ++i) { nk[i] = make_int2(-1, -1); pk_seg[i] = -1; pk_scale[i] = 1.f; }
-#pragma unroll
-  for (int j = 0; j < Sh::NCS; ++j) pcs[j] = make_float2(1.f, 0.f);
+  for (int i = 0; i < Sh::NKU; ++i) {
+    nk[i] = make_int2(-1, -1);
+    cs_seg[i] = -1;
+    k_ok[i] = false;
+    k_scale[i] = 1.f;
+  }
+  nv[0] = nv[1] = make_int2(-1, -1);
+  v_ok[0] = v_ok[1] = false;
+  v_scale[0] = v_scale[1] = 1.f;
 
   const T* ksuf = static_cast<const T*>(a.k_suf);
   const T* vsuf = static_cast<const T*>(a.v_suf);
   const PoolT* kpool = static_cast<const PoolT*>(a.k);
   const PoolT* vpool = static_cast<const PoolT*>(a.v);
-  const int kkv = tid % KT;                 // the key of this thread's value units
+  const int kp2 = 2 * (tid % (KT / 2));    // first of the two keys of this thread's value units
 
   auto fetch_idx = [&](int tile) {
     if (tile >= nct) return;                // suffix tiles need no index
@@ -460,9 +418,11 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         nk[i] = make_int2(-1, -1);
         if (u < Sh::KU_TOT && kk < nvalid) nk[i] = a.slot_info[slot0 + k0 + kk];
       }
-      nv = make_int2(-1, -1);
-      if (kkv < nvalid) nv = a.slot_info[slot0 + k0 + kkv];
-      n_seg0 = a.slot_info[slot0 + k0].y;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        nv[j] = make_int2(-1, -1);
+        if (kp2 + j < nvalid) nv[j] = a.slot_info[slot0 + k0 + kp2 + j];
+      }
     }
   };
 
@@ -476,25 +436,28 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         const int u = tid + i * NT;
         const int kk = u / KUPK, c = u % KUPK;
         uint32_t* w = rk + i * 2 * Sh::WA;
-        if (u < Sh::KU_TOT && kk < nvalid) {
-          const size_t row = (size_t(b) * S + k0 + kk) * a.Hkv + g;
+        k_ok[i] = u < Sh::KU_TOT && kk < nvalid;
+        if (k_ok[i]) {
+          const size_t tok = size_t(b) * S + k0 + kk;
+          const size_t row = tok * a.Hkv + g;
           raw_load8<T>(w, ksuf + row * D + 8 * c);
           raw_load8<T>(w + Sh::WA, ksuf + row * D + 8 * c + HALF);
-        } else {
-          raw_zero8<T>(w);
-          raw_zero8<T>(w + Sh::WA);
+          load_cs8(a.suf_cs + tok * HALF + 8 * c, ck[i], sk[i]);
+          cs_seg[i] = -1;                   // not a pool segment's cos/sin
         }
       }
 #pragma unroll
       for (int i = 0; i < Sh::NVU; ++i) {
         const int u = tid + i * NT;
-        const int c = u / KT;
-        uint32_t* w = rv + i * Sh::WA;
-        if (u < Sh::VU_TOT && kkv < nvalid) {
-          const size_t row = (size_t(b) * S + k0 + kkv) * a.Hkv + g;
-          raw_load8<T>(w, vsuf + row * D + 8 * c);
-        } else {
-          raw_zero8<T>(w);
+        const int c = u / (KT / 2);
+        uint32_t* w = rv + i * 2 * Sh::WA;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          v_ok[j] = u < Sh::VU_TOT && kp2 + j < nvalid;
+          if (v_ok[j]) {
+            const size_t row = (size_t(b) * S + k0 + kp2 + j) * a.Hkv + g;
+            raw_load8<T>(w + j * Sh::WA, vsuf + row * D + 8 * c);
+          }
         }
       }
     } else if constexpr (kPaged) {
@@ -527,48 +490,42 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         const int u = tid + i * NT;
         const int c = u % KUPK;
         uint32_t* w = rk + i * 2 * Sh::WP;
-        pk_seg[i] = nk[i].y;
-        if (nk[i].x >= 0) {
+        k_ok[i] = nk[i].x >= 0;
+        if (k_ok[i]) {
           const size_t row = size_t(nk[i].x) * a.Hkv + g;
           raw_load8<PoolT>(w, kpool + row * D + 8 * c);
           raw_load8<PoolT>(w + Sh::WP, kpool + row * D + 8 * c + HALF);
-          if constexpr (SRC == SRC_POOL_I8) pk_scale[i] = a.k_scale[row];
-        } else {
-          raw_zero8<PoolT>(w);
-          raw_zero8<PoolT>(w + Sh::WP);
+          if constexpr (SRC == SRC_POOL_I8) k_scale[i] = a.k_scale[row];
+          if (nk[i].y != cs_seg[i]) {       // a segment's cos/sin stay until it changes
+            load_cs8(a.seg_cs + size_t(nk[i].y) * HALF + 8 * c, ck[i], sk[i]);
+            cs_seg[i] = nk[i].y;
+          }
         }
       }
-      if (nv.x >= 0) {
-        const size_t row = size_t(nv.x) * a.Hkv + g;
 #pragma unroll
-        for (int i = 0; i < Sh::NVU; ++i) {
-          const int u = tid + i * NT;
-          const int c = u / KT;
-          if (u < Sh::VU_TOT) raw_load8<PoolT>(rv + i * Sh::WP, vpool + row * D + 8 * c);
-          else raw_zero8<PoolT>(rv + i * Sh::WP);
+      for (int i = 0; i < Sh::NVU; ++i) {
+        const int u = tid + i * NT;
+        const int c = u / (KT / 2);
+        uint32_t* w = rv + i * 2 * Sh::WP;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          v_ok[j] = u < Sh::VU_TOT && nv[j].x >= 0;
+          if (v_ok[j]) {
+            const size_t row = size_t(nv[j].x) * a.Hkv + g;
+            raw_load8<PoolT>(w + j * Sh::WP, vpool + row * D + 8 * c);
+            if constexpr (SRC == SRC_POOL_I8) v_scale[j] = a.v_scale[row];
+          }
         }
-        if constexpr (SRC == SRC_POOL_I8) pv_scale = a.v_scale[row];
-      } else {
-#pragma unroll
-        for (int i = 0; i < Sh::NVU; ++i) raw_zero8<PoolT>(rv + i * Sh::WP);
-      }
-      p_seg0 = n_seg0;
-#pragma unroll
-      for (int j = 0; j < Sh::NCS; ++j) {
-        const int e = tid + j * NT;
-        const int seg = n_seg0 + e / HALF;
-        if (e < Sh::CS_TOT && seg < a.n_seg) pcs[j] = a.seg_cs[size_t(seg) * HALF + e % HALF];
       }
     }
   };
 
-  // registers -> LDS (keys turned to their final positions, values transposed)
-  auto commit = [&](int tile) {
+  // registers -> LDS stage (keys turned to their final positions, values transposed)
+  auto commit = [&](int tile, T* sK, T* sV) {
     const bool suffix = tile >= nct;
     const int k0 = suffix ? (tile - nct) * KT : tile * KT;
     const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
     if (suffix || !kPaged) {
-      using RawT = typename std::conditional<kPaged, T, PoolT>::type;
       const bool from_pool = !suffix;
 #pragma unroll
       for (int i = 0; i < Sh::NKU; ++i) {
@@ -576,63 +533,64 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         if (u >= Sh::KU_TOT) continue;
         const int kk = u / KUPK, c = u % KUPK;
         T* dst = sK + kk * L::LDK + 8 * c;
-        float x[8], y[8], cc[8], ss[8];
-        bool valid;
+        if (!k_ok[i]) {
+          store8_zero(dst);
+          store8_zero(dst + HALF);
+          continue;
+        }
+        float x[8], y[8];
         if (from_pool) {
           if constexpr (!kPaged) {
             const uint32_t* w = rk + i * 2 * Sh::WP;
-            valid = pk_seg[i] >= 0;
             raw_to_f8<PoolT>(w, x);
             raw_to_f8<PoolT>(w + Sh::WP, y);
             if constexpr (SRC == SRC_POOL_I8) {
 #pragma unroll
-              for (int e = 0; e < 8; ++e) { x[e] *= pk_scale[i]; y[e] *= pk_scale[i]; }
+              for (int e = 0; e < 8; ++e) { x[e] *= k_scale[i]; y[e] *= k_scale[i]; }
             }
-            if (valid) {
-              const int local = pk_seg[i] - p_seg0;
-              if (local >= 0 && local < NSEG) load_cs8(sCS + local * HALF + 8 * c, cc, ss);
-              else load_cs8(a.seg_cs + size_t(pk_seg[i]) * HALF + 8 * c, cc, ss);
-            }
-          } else {
-            valid = false;
           }
         } else {
           const uint32_t* w = rk + i * 2 * Sh::WA;
-          valid = kk < nvalid;
           raw_to_f8<T>(w, x);
           raw_to_f8<T>(w + Sh::WA, y);
-          if (valid) load_cs8(a.suf_cs + (size_t(b) * S + k0 + kk) * HALF + 8 * c, cc, ss);
         }
-        if (valid) {
-          rotate8(x, y, cc, ss);
-          store8(dst, x);
-          store8(dst + HALF, y);
-        } else {
-          store8_zero(dst);
-          store8_zero(dst + HALF);
-        }
+        rotate8(x, y, ck[i], sk[i]);
+        store8(dst, x);
+        store8(dst + HALF, y);
       }
 #pragma unroll
       for (int i = 0; i < Sh::NVU; ++i) {
         const int u = tid + i * NT;
         if (u >= Sh::VU_TOT) continue;
-        const int c = u / KT;
-        float x[8];
+        const int c = u / (KT / 2);
+        float x0[8], x1[8];
         if (from_pool) {
           if constexpr (!kPaged) {
-            raw_to_f8<PoolT>(rv + i * Sh::WP, x);
+            const uint32_t* w = rv + i * 2 * Sh::WP;
+            raw_to_f8<PoolT>(w, x0);
+            raw_to_f8<PoolT>(w + Sh::WP, x1);
             if constexpr (SRC == SRC_POOL_I8) {
 #pragma unroll
-              for (int e = 0; e < 8; ++e) x[e] *= pv_scale;
+              for (int e = 0; e < 8; ++e) { x0[e] *= v_scale[0]; x1[e] *= v_scale[1]; }
             }
           }
         } else {
-          raw_to_f8<T>(rv + i * Sh::WA, x);
+          const uint32_t* w = rv + i * 2 * Sh::WA;
+          raw_to_f8<T>(w, x0);
+          raw_to_f8<T>(w + Sh::WA, x1);
         }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) sV[(8 * c + e) * L::LDV + kkv] = from_f<T>(x[e]);
+        for (int e = 0; e < 8; ++e) {
+          const float a0 = v_ok[0] ? x0[e] : 0.f;
+          const float a1 = v_ok[1] ? x1[e] : 0.f;
+          T* dst = sV + (8 * c + e) * L::LDV + kp2;
+          if constexpr (sizeof(T) == 2) {
+            *reinterpret_cast<uint32_t*>(dst) = pack_bf16(a0, a1);
+          } else {
+            *reinterpret_cast<float2*>(dst) = make_float2(a0, a1);
+          }
+        }
       }
-      (void)sizeof(RawT);
     } else {
       constexpr int EPV = Sh::EPV;
 #pragma unroll
@@ -650,10 +608,66 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         const int d = u / (KT / EPV), vec = u % (KT / EPV);
         uint4 val = make_uint4(rv[4 * i], rv[4 * i + 1], rv[4 * i + 2], rv[4 * i + 3]);
         if (vec * EPV + EPV > nvalid) val = keep_first<T>(val, nvalid - vec * EPV);
-        *reinterpret_cast<uint4*>(sV + d * L::LDV + vec * EPV) = val;
+        uint2* dst = reinterpret_cast<uint2*>(sV + d * L::LDV + vec * EPV);   // 8-byte aligned rows
+        dst[0] = make_uint2(val.x, val.y);
+        dst[1] = make_uint2(val.z, val.w);
       }
     }
   };
+
+  // ---- Q operand: RoPE at span_end + t, softmax scale and log2(e) folded in.
+  // Lane (qi, half) holds d = c*KSTEP + half*KPL + e in qop[c][e]; the RoPE
+  // partner d + D/2 sits in chunk c + NQC/2 of the same lane.
+  const int t0 = it.tile0, t1 = it.tile1;
+  fetch_idx(t0);
+  Op qop[NQC];
+  {
+    const T* qrow = static_cast<const T*>(a.q) + ((size_t(b) * S + t) * a.Hq + h) * D;
+    const float2* cs = a.suf_cs + (size_t(b) * S + t) * HALF;
+#pragma unroll
+    for (int c = 0; c < NQC / 2; ++c) {
+      const int d0 = c * KSTEP + half * KPL;
+      float x[KPL], y[KPL], cc[KPL], ss[KPL];
+      if (row_ok) {
+        if constexpr (KPL == 8) {
+          uint32_t wx[4], wy[4];
+          raw_load8<T>(wx, qrow + d0);
+          raw_load8<T>(wy, qrow + d0 + HALF);
+          float c8[8], s8[8];
+          raw_to_f8<T>(wx, x);
+          raw_to_f8<T>(wy, y);
+          load_cs8(cs + d0, c8, s8);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) { cc[e] = c8[e]; ss[e] = s8[e]; }
+        } else {
+          x[0] = to_f(qrow[d0]);
+          y[0] = to_f(qrow[d0 + HALF]);
+          const float2 w = cs[d0];
+          cc[0] = w.x;
+          ss[0] = w.y;
+        }
+#pragma unroll
+        for (int e = 0; e < KPL; ++e) {
+          rotate_pair(x[e], y[e], cc[e], ss[e]);
+          x[e] *= a.qscale;
+          y[e] *= a.qscale;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < KPL; ++e) { x[e] = 0.f; y[e] = 0.f; }
+      }
+      if constexpr (KPL == 1) {
+        qop[c] = x[0];
+        qop[c + NQC / 2] = y[0];
+      } else {
+#pragma unroll
+        for (int e = 0; e < KPL; ++e) {
+          qop[c][e] = from_f<T>(x[e]);
+          qop[c + NQC / 2][e] = from_f<T>(y[e]);
+        }
+      }
+    }
+  }
 
   float m_run = kNegInf, l_run = 0.f;
   f32x16 o[NDB];
@@ -662,46 +676,44 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
 
-  const int t0 = it.tile0, t1 = it.tile1;
-  fetch_idx(t0);
+  // prologue: tile t0 into stage 0, tile t0 + 1 in registers
   fetch_data(t0);
   if (t0 + 1 < t1) fetch_idx(t0 + 1);
+  commit(t0, sbuf, sbuf + KT * L::LDK);
+  if (t0 + 1 < t1) fetch_data(t0 + 1);
+  if (t0 + 2 < t1) fetch_idx(t0 + 2);
+  __syncthreads();
 
   for (int tile = t0; tile < t1; ++tile) {
+    const int stage = (tile - t0) & 1;
+    const T* sK = sbuf + stage * L::TILE;
+    const T* sV = sK + KT * L::LDK;
     const bool suffix = tile >= nct;
     const int k0 = suffix ? (tile - nct) * KT : tile * KT;
     const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
 
-    if constexpr (!kPaged) {
-      // every read of the previous tile's cos/sin cache finished before the
-      // barrier that preceded the previous compute
-      if (!suffix) {
-#pragma unroll
-        for (int j = 0; j < Sh::NCS; ++j) {
-          const int e = tid + j * NT;
-          if (e < Sh::CS_TOT) sCS[e] = pcs[j];
-        }
-      }
+    // next tile into the other stage; its readers finished before the last barrier
+    if (tile + 1 < t1) {
+      T* nK = sbuf + (stage ^ 1) * L::TILE;
+      commit(tile + 1, nK, nK + KT * L::LDK);
+      if (tile + 2 < t1) fetch_data(tile + 2);
+      if (tile + 3 < t1) fetch_idx(tile + 3);
     }
-    __syncthreads();   // previous tile consumed; cos/sin cache visible
-    commit(tile);
-    __syncthreads();
-    if (tile + 1 < t1) fetch_data(tile + 1);
-    if (tile + 2 < t1) fetch_idx(tile + 2);
 
-    // ---- S^T = K Q^T: two 32-key blocks, accumulator lane = query
-    f32x16 s[2];
+    // ---- S^T = K Q^T over this wavefront's 32-key blocks, accumulator lane = query
+    f32x16 s[NKB];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int j = 0; j < NKB; ++j) {
+      const int kb = kh * NKB + j;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
+      for (int v = 0; v < 16; ++v) s[j][v] = 0.f;
       const T* krow = sK + (kb * 32 + qi) * L::LDK + half * KPL;
 #pragma unroll
       for (int c = 0; c < NQC; ++c) {
         Op ka;
         if constexpr (KPL == 1) ka = krow[c * KSTEP];
         else ka = *reinterpret_cast<const Op*>(krow + c * KSTEP);
-        s[kb] = M::run(ka, qop[c], s[kb]);
+        s[j] = M::run(ka, qop[c], s[j]);
       }
     }
 
@@ -709,29 +721,29 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
     // holds key 32*kb + 8*(v/4) + 4*half + v%4 of the tile
     if (suffix || nvalid < KT) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int j = 0; j < NKB; ++j)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int key = kb * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+          const int key = (kh * NKB + j) * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
           const bool vis = key < nvalid && (!suffix || k0 + key <= t);
-          if (!vis) s[kb][v] = kNegInf;
+          if (!vis) s[j][v] = kNegInf;
         }
     }
     float mt = kNegInf;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int j = 0; j < NKB; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s[kb][v]);
+      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s[j][v]);
     mt = fmaxf(mt, __shfl_xor(mt, 32));
     const float m_new = fmaxf(m_run, mt);
     const float m_ref = (m_new == kNegInf) ? 0.f : m_new;
     float psum = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int j = 0; j < NKB; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(s[kb][v] - m_ref);
-        s[kb][v] = p;
+        const float p = __builtin_amdgcn_exp2f(s[j][v] - m_ref);
+        s[j][v] = p;
         psum += p;
       }
     if (__any(m_new > m_run)) {
@@ -748,15 +760,17 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
     // ---- O^T += V^T P^T.  Chunk c takes accumulator values
     // v = KPL*(c % CPB) + e of block c / CPB; the matching key is read from sV.
 #pragma unroll
-    for (int c = 0; c < NPC; ++c) {
+    for (int cc = 0; cc < NPC / KG; ++cc) {
+      const int c = kh * (NPC / KG) + cc;
+      const int j = cc / CPB;
       const int kb = c / CPB;
       const int v0 = KPL * (c % CPB);
       Op pb;
       if constexpr (KPL == 1) {
-        pb = s[kb][v0];
+        pb = s[j][v0];
       } else {
 #pragma unroll
-        for (int e = 0; e < KPL; ++e) pb[e] = from_f<T>(s[kb][v0 + e]);
+        for (int e = 0; e < KPL; ++e) pb[e] = from_f<T>(s[j][v0 + e]);
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
@@ -774,13 +788,45 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         o[db] = M::run(va, pb, o[db]);
       }
     }
+    __syncthreads();   // next stage written; this stage free for the tile after next
   }
+
+  // ---- the two key halves of a row group combine (same lane, same rows)
+  if constexpr (KG == 2) {
+    constexpr int XW = 2 + NDB * 16;                     // m, l and this lane's outputs
+    static_assert(NRG * 64 * XW * sizeof(float) <= 2 * L::TILE * sizeof(T),
+                  "key-half exchange must fit in the tile stages");
+    float* xs = reinterpret_cast<float*>(sbuf);          // [NRG][64 lanes][XW] floats
+    float* mine = xs + (size_t(rgrp) * 64 + lane) * XW;
+    if (kh == 1) {
+      mine[0] = m_run;
+      mine[1] = l_run;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mine[2 + db * 16 + v] = o[db][v];
+    }
+    __syncthreads();
+    if (kh == 0) {
+      const float m1 = mine[0], l1 = mine[1];
+      const float mx = fmaxf(m_run, m1);
+      const float mr = (mx == kNegInf) ? 0.f : mx;
+      const float a0 = __builtin_amdgcn_exp2f(m_run - mr), a1 = __builtin_amdgcn_exp2f(m1 - mr);
+      l_run = l_run * a0 + l1 * a1;
+      m_run = mx;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) o[db][v] = o[db][v] * a0 + mine[2 + db * 16 + v] * a1;
+    }
+  }
+  const bool writer = KG == 1 || kh == 0;
 
   // ---- epilogue: accumulator value v of block db holds d = 32*db + 8*(v/4) + 4*half + v%4
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float lse_val = l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2 : kNegInf;
-  if (row_ok) {
+  if (row_ok && writer) {
     if (it.partial < 0) {
       T* orow = static_cast<T*>(a.out) + ((size_t(b) * S + t) * a.Hq + h) * D;
 #pragma unroll
@@ -926,8 +972,10 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
   constexpr int VV = KT / EPV;
   for (int u = threadIdx.x; u < D * VV; u += blockDim.x) {
     const int d = u / VV, vec = u % VV;
+    const uint2* src = reinterpret_cast<const uint2*>(sV + d * L::LDV + vec * EPV);
+    const uint2 lo = src[0], hi = src[1];     // LDS rows are 8-byte aligned
     *reinterpret_cast<uint4*>(vpage + size_t(d) * a.PS + vec * EPV) =
-        *reinterpret_cast<const uint4*>(sV + d * L::LDV + vec * EPV);
+        make_uint4(lo.x, lo.y, hi.x, hi.y);
   }
 }
 
@@ -936,6 +984,17 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
 // ----------------------------------------------------------------------------
 
 namespace {
+
+// Launch `kernel(params)`.  With timing events, the dispatch packet itself
+// stamps them at kernel start and end (hipExtLaunchKernel), the same
+// timestamps a kernel trace reports.
+template <typename P>
+hipError_t launch(const void* kernel, dim3 grid, dim3 block, hipStream_t st, const P& params,
+                  hipEvent_t ev0, hipEvent_t ev1) {
+  void* args[] = {const_cast<P*>(&params)};
+  if (ev0 || ev1) return hipExtLaunchKernel(kernel, grid, block, args, 0, st, ev0, ev1, 0);
+  return hipLaunchKernel(kernel, grid, block, args, 0, st);
+}
 
 template <typename T>
 const T* at(const void* base, size_t off) {
@@ -947,18 +1006,18 @@ T* at_mut(void* base, size_t off) {
 }
 
 template <typename T, int D, int SRC>
-hipError_t launch_attn_t(const AttnParams& ap, int n_items, int threads, hipStream_t st) {
-  if (threads == 512)
-    hipLaunchKernelGGL((attn_kernel<T, D, SRC, 512>), dim3(n_items), dim3(512), 0, st, ap);
-  else
-    hipLaunchKernelGGL((attn_kernel<T, D, SRC, 256>), dim3(n_items), dim3(256), 0, st, ap);
-  return hipGetLastError();
+hipError_t launch_attn_t(const AttnParams& ap, int n_items, int rows, hipStream_t st,
+                         hipEvent_t e0, hipEvent_t e1) {
+  const void* k = rows == 256 ? reinterpret_cast<const void*>(&attn_kernel<T, D, SRC, 1>)
+                              : reinterpret_cast<const void*>(&attn_kernel<T, D, SRC, 2>);
+  return launch(k, dim3(n_items), dim3(512), st, ap, e0, e1);
 }
 
 template <typename T, int SRC>
-hipError_t launch_attn_d(int D, const AttnParams& ap, int n, int threads, hipStream_t st) {
-  return D == 64 ? launch_attn_t<T, 64, SRC>(ap, n, threads, st)
-                 : launch_attn_t<T, 128, SRC>(ap, n, threads, st);
+hipError_t launch_attn_d(int D, const AttnParams& ap, int n, int rows, hipStream_t st,
+                         hipEvent_t e0, hipEvent_t e1) {
+  return D == 64 ? launch_attn_t<T, 64, SRC>(ap, n, rows, st, e0, e1)
+                 : launch_attn_t<T, 128, SRC>(ap, n, rows, st, e0, e1);
 }
 
 }  // namespace
@@ -966,7 +1025,7 @@ hipError_t launch_attn_d(int D, const AttnParams& ap, int n, int threads, hipStr
 hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const void* v,
                             const float* k_scale, const float* v_scale, const void* q,
                             const void* k_suf, const void* v_suf, void* out, float* lse,
-                            hipStream_t st) {
+                            hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   void* ws = p.d_workspace;
   AttnParams ap{};
   ap.Hq = p.cfg.n_q_heads;
@@ -999,18 +1058,19 @@ hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const vo
   ap.part_o = at_mut<float>(ws, p.ws.part_o);
   ap.part_lse = at_mut<float>(ws, p.ws.part_lse);
   const int n = static_cast<int>(p.items.size());
-  const int threads = 64 * (p.rows_per_block / kRowsPerWave);
+  const int rows = p.rows_per_block;      // selects the row-block shape
   const int D = p.cfg.head_dim;
   if (p.cfg.act_dtype == C2KV_F32) {
-    if (src_kind == SRC_PAGED) return launch_attn_d<float, SRC_PAGED>(D, ap, n, threads, st);
-    return launch_attn_d<float, SRC_POOL>(D, ap, n, threads, st);
+    if (src_kind == SRC_PAGED) return launch_attn_d<float, SRC_PAGED>(D, ap, n, rows, st, e0, e1);
+    return launch_attn_d<float, SRC_POOL>(D, ap, n, rows, st, e0, e1);
   }
-  if (src_kind == SRC_PAGED) return launch_attn_d<__bf16, SRC_PAGED>(D, ap, n, threads, st);
-  if (src_kind == SRC_POOL) return launch_attn_d<__bf16, SRC_POOL>(D, ap, n, threads, st);
-  return launch_attn_d<__bf16, SRC_POOL_I8>(D, ap, n, threads, st);
+  if (src_kind == SRC_PAGED) return launch_attn_d<__bf16, SRC_PAGED>(D, ap, n, rows, st, e0, e1);
+  if (src_kind == SRC_POOL) return launch_attn_d<__bf16, SRC_POOL>(D, ap, n, rows, st, e0, e1);
+  return launch_attn_d<__bf16, SRC_POOL_I8>(D, ap, n, rows, st, e0, e1);
 }
 
-hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st) {
+hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st, hipEvent_t e0,
+                        hipEvent_t e1) {
   if (p.merges.empty() || p.merge_in_kernel) return hipSuccess;
   MergeParams mp{};
   mp.Hq = p.cfg.n_q_heads;
@@ -1025,20 +1085,20 @@ hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st) {
   const int D = p.cfg.head_dim;
   const int rpw = 256 / (D / 4);
   const dim3 grid(static_cast<unsigned>(p.merges.size()), (p.rows_per_block + rpw - 1) / rpw);
-  if (p.cfg.act_dtype == C2KV_F32) {
-    if (D == 64) hipLaunchKernelGGL((merge_kernel<float, 64>), grid, dim3(256), 0, st, mp);
-    else hipLaunchKernelGGL((merge_kernel<float, 128>), grid, dim3(256), 0, st, mp);
-  } else {
-    if (D == 64) hipLaunchKernelGGL((merge_kernel<__bf16, 64>), grid, dim3(256), 0, st, mp);
-    else hipLaunchKernelGGL((merge_kernel<__bf16, 128>), grid, dim3(256), 0, st, mp);
-  }
-  return hipGetLastError();
+  const void* k;
+  if (p.cfg.act_dtype == C2KV_F32)
+    k = D == 64 ? reinterpret_cast<const void*>(&merge_kernel<float, 64>)
+                : reinterpret_cast<const void*>(&merge_kernel<float, 128>);
+  else
+    k = D == 64 ? reinterpret_cast<const void*>(&merge_kernel<__bf16, 64>)
+                : reinterpret_cast<const void*>(&merge_kernel<__bf16, 128>);
+  return launch(k, grid, dim3(256), st, mp, e0, e1);
 }
 
 hipError_t launch_compose(const Plan& p, int pool_dtype, const void* k, const void* v,
                           const float* k_scale, const float* v_scale, void* k_pages,
                           void* v_pages, int64_t* out_src_row, int32_t* out_pos,
-                          hipStream_t st) {
+                          hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
   const int n_tiles = static_cast<int>(p.compose_tiles.size() / 2);
   if (n_tiles == 0) return hipSuccess;
   ComposeParams cp{};
@@ -1061,17 +1121,17 @@ hipError_t launch_compose(const Plan& p, int pool_dtype, const void* k, const vo
   cp.out_pos = out_pos;
   const dim3 grid(n_tiles, p.cfg.n_kv_heads);
   const int D = p.cfg.head_dim;
-  if (p.cfg.act_dtype == C2KV_F32) {
-    if (D == 64) hipLaunchKernelGGL((compose_kernel<float, 64, float>), grid, dim3(256), 0, st, cp);
-    else hipLaunchKernelGGL((compose_kernel<float, 128, float>), grid, dim3(256), 0, st, cp);
-  } else if (pool_dtype == C2KV_I8) {
-    if (D == 64) hipLaunchKernelGGL((compose_kernel<__bf16, 64, int8_t>), grid, dim3(256), 0, st, cp);
-    else hipLaunchKernelGGL((compose_kernel<__bf16, 128, int8_t>), grid, dim3(256), 0, st, cp);
-  } else {
-    if (D == 64) hipLaunchKernelGGL((compose_kernel<__bf16, 64, __bf16>), grid, dim3(256), 0, st, cp);
-    else hipLaunchKernelGGL((compose_kernel<__bf16, 128, __bf16>), grid, dim3(256), 0, st, cp);
-  }
-  return hipGetLastError();
+  const void* k_;
+  if (p.cfg.act_dtype == C2KV_F32)
+    k_ = D == 64 ? reinterpret_cast<const void*>(&compose_kernel<float, 64, float>)
+                 : reinterpret_cast<const void*>(&compose_kernel<float, 128, float>);
+  else if (pool_dtype == C2KV_I8)
+    k_ = D == 64 ? reinterpret_cast<const void*>(&compose_kernel<__bf16, 64, int8_t>)
+                 : reinterpret_cast<const void*>(&compose_kernel<__bf16, 128, int8_t>);
+  else
+    k_ = D == 64 ? reinterpret_cast<const void*>(&compose_kernel<__bf16, 64, __bf16>)
+                 : reinterpret_cast<const void*>(&compose_kernel<__bf16, 128, __bf16>);
+  return launch(k_, grid, dim3(256), st, cp, e0, e1);
 }
 
 }  // namespace c2kv

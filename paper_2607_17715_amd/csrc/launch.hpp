@@ -1,4 +1,5 @@
 // Kernel launchers (defined in kernels.hip), called by the C ABI in api.cpp.
+// Non-null events are stamped at the kernel's start and end.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -12,11 +13,12 @@ enum SrcKind { kSrcPaged = 0, kSrcPool = 1, kSrcPoolI8 = 2 };
 hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const void* v,
                             const float* k_scale, const float* v_scale, const void* q,
                             const void* k_suf, const void* v_suf, void* out, float* lse,
-                            hipStream_t st);
-hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st);
+                            hipStream_t st, hipEvent_t e0, hipEvent_t e1);
+hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st, hipEvent_t e0,
+                        hipEvent_t e1);
 hipError_t launch_compose(const Plan& p, int pool_dtype, const void* k, const void* v,
                           const float* k_scale, const float* v_scale, void* k_pages,
                           void* v_pages, int64_t* out_src_row, int32_t* out_pos,
-                          hipStream_t st);
+                          hipStream_t st, hipEvent_t e0, hipEvent_t e1);
 
 }  // namespace c2kv

@@ -220,7 +220,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   int RB = o.rows_per_block;
   if (RB == 0) RB = R >= 256 ? 256 : 128;
   p.rows_per_block = RB;
-  const int wgs_per_cu = RB >= 256 ? 1 : 2;
+  const int wgs_per_cu = 1;           // 8 wavefronts at 2 per SIMD fill a CU
   const int64_t target = int64_t(o.num_cus) * wgs_per_cu;
   const int32_t n_rb = ceil_div(R, RB);
   struct Group { int32_t b, g, row0, nrows, tiles; };
@@ -255,7 +255,8 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
     for (int s = 0; s < ns; ++s) {
       const int32_t t0 = static_cast<int32_t>(int64_t(gr.tiles) * s / ns);
       const int32_t t1 = static_cast<int32_t>(int64_t(gr.tiles) * (s + 1) / ns);
-      items.push_back({gr.b, gr.g, gr.row0, gr.nrows, t0, t1, ns > 1 ? part0 + s : -1, merge});
+      items.push_back({gr.b, gr.g, gr.row0, gr.nrows, t0, t1, ns > 1 ? part0 + s : -1, merge,
+                       p.req_slot0[gr.b], p.req_slot0[gr.b + 1] - p.req_slot0[gr.b], 0, 0});
     }
   }
   p.merge_in_kernel = o.merge_mode == 1 || (o.merge_mode == 0 && p.max_splits <= 8);
