@@ -15,7 +15,8 @@ from typing import Optional
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libc2kv.so")
+# C2KV_LIBRARY selects another build of the same library (e.g. one with extra flags)
+LIB_PATH = os.environ.get("C2KV_LIBRARY") or os.path.join(_PKG, "libc2kv.so")
 
 C2KV_OK, C2KV_E_INVAL, C2KV_E_UNSUPPORTED, C2KV_E_WORKSPACE, C2KV_E_HIP, C2KV_E_NOMEM, \
     C2KV_E_STATE = 0, -1, -2, -3, -4, -5, -6

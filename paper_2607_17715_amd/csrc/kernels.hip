@@ -141,6 +141,21 @@ template <> struct Mma<__bf16> {
   }
 };
 
+// maximum of x over lanes l and l ^ 32, a VALU lane swap: the swap's first
+// result holds the lower half's values in every lane, the second the upper's
+__device__ inline float half_pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// sum of x over lanes l and l ^ 32, the same value (same operand order) in both
+__device__ inline float half_pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // ----------------------------------------------------------------------------
 // raw 32-bit words of 8 consecutive elements (2 * sizeof(S) words)
 // ----------------------------------------------------------------------------
@@ -224,7 +239,7 @@ struct AttnParams {
   const void* v_suf;
   void* out;
   float* lse;
-  float* part_o;
+  void* part_o;                 // [n_partials][RB][D], activation dtype
   float* part_lse;
 };
 
@@ -249,7 +264,7 @@ struct ComposeParams {
 struct MergeParams {
   int Hq, G, S, RB;
   const MergeGroup* groups;
-  const float* part_o;
+  const void* part_o;
   const float* part_lse;
   void* out;
   float* lse;
@@ -290,7 +305,7 @@ struct Shape {
 // ----------------------------------------------------------------------------
 
 template <typename T, int D>
-__device__ inline void merge_rows(const MergeGroup& mg, int rlo, int rhi, const float* part_o,
+__device__ inline void merge_rows(const MergeGroup& mg, int rlo, int rhi, const void* part_o,
                                   const float* part_lse, int RB, int Hq, int G, int S,
                                   void* out, float* lse, int tid, int nthr) {
   constexpr int TPR = D / 4;
@@ -298,7 +313,7 @@ __device__ inline void merge_rows(const MergeGroup& mg, int rlo, int rhi, const 
     const int rloc = rlo + idx / TPR;
     const int d = 4 * (idx % TPR);
     const float* pl = part_lse + size_t(mg.part0) * RB + rloc;
-    const float* po = part_o + (size_t(mg.part0) * RB + rloc) * D + d;
+    const T* po = static_cast<const T*>(part_o) + (size_t(mg.part0) * RB + rloc) * D + d;
     float mx = kNegInf;
 #pragma unroll 8
     for (int i = 0; i < mg.nsplit; ++i) mx = fmaxf(mx, pl[size_t(i) * RB]);
@@ -308,7 +323,14 @@ __device__ inline void merge_rows(const MergeGroup& mg, int rlo, int rhi, const 
     for (int i = 0; i < mg.nsplit; ++i) {
       const float li = pl[size_t(i) * RB];
       const float w = (li == kNegInf) ? 0.f : __expf(li - mx);
-      const float4 v = *reinterpret_cast<const float4*>(po + size_t(i) * RB * D);
+      float4 v;
+      if constexpr (sizeof(T) == 4) {
+        v = *reinterpret_cast<const float4*>(po + size_t(i) * RB * D);
+      } else {
+        const uint2 u = *reinterpret_cast<const uint2*>(po + size_t(i) * RB * D);
+        v = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                        __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+      }
       z += w;
       acc.x += w * v.x; acc.y += w * v.y; acc.z += w * v.z; acc.w += w * v.w;
     }
@@ -333,52 +355,29 @@ __device__ inline void merge_rows(const MergeGroup& mg, int rlo, int rhi, const 
 // attention
 // ----------------------------------------------------------------------------
 
-// One workgroup = 8 wavefronts.  With KG = 1 each wavefront owns 32 query rows
-// (256 per workgroup) and every key of a tile; with KG = 2 four row groups of
-// 32 rows (128 per workgroup) each see one half of every 64-key tile, keep their
-// own online softmax, and the two halves are combined through LDS at the end.
-template <typename T, int D, int SRC, int KG>
-__global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
-  constexpr int NT = 512;
-  constexpr int NRG = 8 / KG;               // row groups
-  constexpr int NKB = 2 / KG;               // 32-key blocks per wavefront and tile
-  using M = Mma<T>;
-  using Op = typename M::Op;
-  using L = Lds<T, D>;
+// Loads key tiles of one workgroup through registers into LDS.  Slot indices
+// are fetched two tiles ahead of use and row data one tile ahead; `commit`
+// turns keys to their final positions (decoding int8 first) and writes them row
+// by row into sK[KT][LDK], and writes values transposed into sV[D][LDV].
+// Cached tiles come from the pool (gather) or from pages; suffix tiles from
+// k_suf / v_suf, with RoPE at span_end + u.
+template <typename T, int D, int SRC, int NT>
+struct TileLoader {
   using PoolT = typename std::conditional<SRC == SRC_POOL_I8, int8_t, T>::type;
-  constexpr bool kPaged = SRC == SRC_PAGED;
+  static constexpr bool kPaged = SRC == SRC_PAGED;
   using Sh = Shape<T, PoolT, D, NT, kPaged>;
-  constexpr int KPL = M::KPL;
-  constexpr int KSTEP = 2 * KPL;            // contraction length of one MFMA
-  constexpr int NQC = D / KSTEP;            // Q operand chunks over d
-  constexpr int NDB = D / 32;               // 32-wide d blocks of the output
-  constexpr int CPB = 32 / KSTEP;           // P*V chunks per 32-key block
-  constexpr int NPC = KT / KSTEP;           // P*V chunks per key tile
-  constexpr int HALF = D / 2;
-  constexpr int KUPK = D / 16;              // key units per key
+  using L = Lds<T, D>;
+  static constexpr int HALF = D / 2;
+  static constexpr int KUPK = D / 16;       // key units per key
 
-  // two stages of [keys | transposed values]
-  __shared__ __attribute__((aligned(16))) T sbuf[2 * L::TILE];
-  __shared__ int s_last;
+  const AttnParams& a;
+  const int tid, b, g, S, slot0, N, nct;
+  const int kp2;                            // first of the two keys of this thread's value units
+  const T* ksuf;
+  const T* vsuf;
+  const PoolT* kpool;
+  const PoolT* vpool;
 
-  const int tid = threadIdx.x;
-  const WorkItem it = a.items[blockIdx.x];
-  const int wave = tid >> 6, lane = tid & 63;
-  const int qi = lane & 31, half = lane >> 5;
-  const int b = it.b, g = it.g;
-  const int S = a.S, G = a.G;
-  const int slot0 = it.slot0;
-  const int N = it.nslots;
-  const int nct = (N + KT - 1) / KT;
-
-  const int rgrp = wave % NRG, kh = wave / NRG;
-  const int rloc = rgrp * 32 + qi;
-  const bool row_ok = rloc < it.nrows;
-  const int r = it.row0 + rloc;
-  const int t = row_ok ? r / G : 0;
-  const int h = g * G + (row_ok ? r % G : 0);
-
-  // ---- tile pipeline state: indices two tiles ahead, data one tile ahead ----
   uint32_t rk[Sh::RKW], rv[Sh::RVW];
   float ck[Sh::NKU][8], sk[Sh::NKU][8];     // cos/sin of this thread's key units
   int cs_seg[Sh::NKU];                      // segment the pool cos/sin belong to
@@ -387,24 +386,26 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
   bool k_ok[Sh::NKU];
   bool v_ok[2];
   float k_scale[Sh::NKU], v_scale[2];
+
+  __device__ __forceinline__ TileLoader(const AttnParams& a_, int tid_, int b_, int g_, int slot0_,
+                                        int N_)
+      : a(a_), tid(tid_), b(b_), g(g_), S(a_.S), slot0(slot0_), N(N_), nct((N_ + KT - 1) / KT),
+        kp2(2 * (tid_ % (KT / 2))), ksuf(static_cast<const T*>(a_.k_suf)),
+        vsuf(static_cast<const T*>(a_.v_suf)), kpool(static_cast<const PoolT*>(a_.k)),
+        vpool(static_cast<const PoolT*>(a_.v)) {
 #pragma unroll
-  for (int i = 0; i < Sh::NKU; ++i) {
-    nk[i] = make_int2(-1, -1);
-    cs_seg[i] = -1;
-    k_ok[i] = false;
-    k_scale[i] = 1.f;
+    for (int i = 0; i < Sh::NKU; ++i) {
+      nk[i] = make_int2(-1, -1);
+      cs_seg[i] = -1;
+      k_ok[i] = false;
+      k_scale[i] = 1.f;
+    }
+    nv[0] = nv[1] = make_int2(-1, -1);
+    v_ok[0] = v_ok[1] = false;
+    v_scale[0] = v_scale[1] = 1.f;
   }
-  nv[0] = nv[1] = make_int2(-1, -1);
-  v_ok[0] = v_ok[1] = false;
-  v_scale[0] = v_scale[1] = 1.f;
 
-  const T* ksuf = static_cast<const T*>(a.k_suf);
-  const T* vsuf = static_cast<const T*>(a.v_suf);
-  const PoolT* kpool = static_cast<const PoolT*>(a.k);
-  const PoolT* vpool = static_cast<const PoolT*>(a.v);
-  const int kp2 = 2 * (tid % (KT / 2));    // first of the two keys of this thread's value units
-
-  auto fetch_idx = [&](int tile) {
+  __device__ __forceinline__ void fetch_idx(int tile) {
     if (tile >= nct) return;                // suffix tiles need no index
     const int k0 = tile * KT;
     const int nvalid = min(KT, N - k0);
@@ -424,9 +425,9 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
         if (kp2 + j < nvalid) nv[j] = a.slot_info[slot0 + k0 + kp2 + j];
       }
     }
-  };
+  }
 
-  auto fetch_data = [&](int tile) {
+  __device__ __forceinline__ void fetch_data(int tile) {
     const bool suffix = tile >= nct;
     const int k0 = suffix ? (tile - nct) * KT : tile * KT;
     const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
@@ -518,10 +519,9 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
         }
       }
     }
-  };
+  }
 
-  // registers -> LDS stage (keys turned to their final positions, values transposed)
-  auto commit = [&](int tile, T* sK, T* sV) {
+  __device__ __forceinline__ void commit(int tile, T* sK, T* sV) {
     const bool suffix = tile >= nct;
     const int k0 = suffix ? (tile - nct) * KT : tile * KT;
     const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
@@ -613,42 +613,109 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
         dst[1] = make_uint2(val.z, val.w);
       }
     }
-  };
+  }
+};
+
+// One workgroup = 8 wavefronts.  With KG = 1 each wavefront owns 32 query rows
+// (256 per workgroup) and every key of a tile; with KG = 2 four row groups of
+// 32 rows (128 per workgroup) each see one half of every 64-key tile, keep their
+// own online softmax, and the two halves are combined through LDS at the end.
+template <typename T, int D, int SRC, int KG>
+__global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
+  constexpr int NT = 512;
+  constexpr int NRG = 8 / KG;               // row groups
+  constexpr int NKB = 2 / KG;               // 32-key blocks per wavefront and tile
+  using M = Mma<T>;
+  using Op = typename M::Op;
+  using L = Lds<T, D>;
+  using PoolT = typename std::conditional<SRC == SRC_POOL_I8, int8_t, T>::type;
+  constexpr bool kPaged = SRC == SRC_PAGED;
+  using Sh = Shape<T, PoolT, D, NT, kPaged>;
+  constexpr int KPL = M::KPL;
+  constexpr int KSTEP = 2 * KPL;            // contraction length of one MFMA
+  constexpr int NQC = D / KSTEP;            // Q operand chunks over d
+  constexpr int NDB = D / 32;               // 32-wide d blocks of the output
+  constexpr int CPB = 32 / KSTEP;           // P*V chunks per 32-key block
+  constexpr int NPC = KT / KSTEP;           // P*V chunks per key tile
+  constexpr int HALF = D / 2;
+  constexpr int KUPK = D / 16;              // key units per key
+
+  // two stages of [keys | transposed values]
+  constexpr int SBUF = 2 * L::TILE;
+  __shared__ __attribute__((aligned(16))) T sbuf[SBUF];
+  __shared__ int s_last;
+  auto kst = [&](int i) { return sbuf + i * L::TILE; };
+  auto vst = [&](int i) { return sbuf + i * L::TILE + KT * L::LDK; };
+
+  const int tid = threadIdx.x;
+  const WorkItem it = a.items[blockIdx.x];
+  const int wave = tid >> 6, lane = tid & 63;
+  const int qi = lane & 31, half = lane >> 5;
+  const int b = it.b, g = it.g;
+  const int S = a.S, G = a.G;
+  const int slot0 = it.slot0;
+  const int N = it.nslots;
+  const int nct = (N + KT - 1) / KT;
+
+  const int rgrp = wave % NRG, kh = wave / NRG;
+  const int rloc = rgrp * 32 + qi;
+  const bool row_ok = rloc < it.nrows;
+  const int r = it.row0 + rloc;
+  const int t = row_ok ? r / G : 0;
+  const int h = g * G + (row_ok ? r % G : 0);
+
+  TileLoader<T, D, SRC, NT> ld(a, tid, b, g, slot0, N);
+  auto fetch_idx = [&](int tile) { ld.fetch_idx(tile); };
+  auto fetch_data = [&](int tile) { ld.fetch_data(tile); };
+  auto commit = [&](int tile, T* sK, T* sV) { ld.commit(tile, sK, sV); };
 
   // ---- Q operand: RoPE at span_end + t, softmax scale and log2(e) folded in.
   // Lane (qi, half) holds d = c*KSTEP + half*KPL + e in qop[c][e]; the RoPE
   // partner d + D/2 sits in chunk c + NQC/2 of the same lane.
+  // The Q and cos/sin loads are issued first, then the first key tile's row
+  // loads (whose addresses wait only for the slot indices), and only then is Q
+  // rotated, so the two latencies overlap.
   const int t0 = it.tile0, t1 = it.tile1;
   fetch_idx(t0);
   Op qop[NQC];
   {
     const T* qrow = static_cast<const T*>(a.q) + ((size_t(b) * S + t) * a.Hq + h) * D;
     const float2* cs = a.suf_cs + (size_t(b) * S + t) * HALF;
+    constexpr int NW = KPL == 8 ? 4 : 1;                 // raw words per KPL elements
+    uint32_t qx[NQC / 2][NW], qy[NQC / 2][NW];
+    float qc[NQC / 2][KPL], qs[NQC / 2][KPL];
 #pragma unroll
     for (int c = 0; c < NQC / 2; ++c) {
       const int d0 = c * KSTEP + half * KPL;
-      float x[KPL], y[KPL], cc[KPL], ss[KPL];
       if (row_ok) {
         if constexpr (KPL == 8) {
-          uint32_t wx[4], wy[4];
-          raw_load8<T>(wx, qrow + d0);
-          raw_load8<T>(wy, qrow + d0 + HALF);
-          float c8[8], s8[8];
-          raw_to_f8<T>(wx, x);
-          raw_to_f8<T>(wy, y);
-          load_cs8(cs + d0, c8, s8);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) { cc[e] = c8[e]; ss[e] = s8[e]; }
+          raw_load8<T>(qx[c], qrow + d0);
+          raw_load8<T>(qy[c], qrow + d0 + HALF);
+          load_cs8(cs + d0, qc[c], qs[c]);
         } else {
-          x[0] = to_f(qrow[d0]);
-          y[0] = to_f(qrow[d0 + HALF]);
+          qx[c][0] = __float_as_uint(to_f(qrow[d0]));
+          qy[c][0] = __float_as_uint(to_f(qrow[d0 + HALF]));
           const float2 w = cs[d0];
-          cc[0] = w.x;
-          ss[0] = w.y;
+          qc[c][0] = w.x;
+          qs[c][0] = w.y;
+        }
+      }
+    }
+    fetch_data(t0);
+#pragma unroll
+    for (int c = 0; c < NQC / 2; ++c) {
+      float x[KPL], y[KPL];
+      if (row_ok) {
+        if constexpr (KPL == 8) {
+          raw_to_f8<T>(qx[c], x);
+          raw_to_f8<T>(qy[c], y);
+        } else {
+          x[0] = __uint_as_float(qx[c][0]);
+          y[0] = __uint_as_float(qy[c][0]);
         }
 #pragma unroll
         for (int e = 0; e < KPL; ++e) {
-          rotate_pair(x[e], y[e], cc[e], ss[e]);
+          rotate_pair(x[e], y[e], qc[c][e], qs[c][e]);
           x[e] *= a.qscale;
           y[e] *= a.qscale;
         }
@@ -676,32 +743,8 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
 
-  // prologue: tile t0 into stage 0, tile t0 + 1 in registers
-  fetch_data(t0);
-  if (t0 + 1 < t1) fetch_idx(t0 + 1);
-  commit(t0, sbuf, sbuf + KT * L::LDK);
-  if (t0 + 1 < t1) fetch_data(t0 + 1);
-  if (t0 + 2 < t1) fetch_idx(t0 + 2);
-  __syncthreads();
-
-  for (int tile = t0; tile < t1; ++tile) {
-    const int stage = (tile - t0) & 1;
-    const T* sK = sbuf + stage * L::TILE;
-    const T* sV = sK + KT * L::LDK;
-    const bool suffix = tile >= nct;
-    const int k0 = suffix ? (tile - nct) * KT : tile * KT;
-    const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
-
-    // next tile into the other stage; its readers finished before the last barrier
-    if (tile + 1 < t1) {
-      T* nK = sbuf + (stage ^ 1) * L::TILE;
-      commit(tile + 1, nK, nK + KT * L::LDK);
-      if (tile + 2 < t1) fetch_data(tile + 2);
-      if (tile + 3 < t1) fetch_idx(tile + 3);
-    }
-
-    // ---- S^T = K Q^T over this wavefront's 32-key blocks, accumulator lane = query
-    f32x16 s[NKB];
+  // ---- S^T = K Q^T over this wavefront's 32-key blocks, accumulator lane = query
+  auto qk = [&](const T* sK, f32x16 (&s)[NKB]) {
 #pragma unroll
     for (int j = 0; j < NKB; ++j) {
       const int kb = kh * NKB + j;
@@ -716,9 +759,14 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
         s[j] = M::run(ka, qop[c], s[j]);
       }
     }
+  };
 
-    // ---- mask and online softmax (base 2); accumulator value v of block kb
-    // holds key 32*kb + 8*(v/4) + 4*half + v%4 of the tile
+  // ---- causal / ragged-tail mask, then the new running maximum (base 2);
+  // accumulator value v of block kb holds key 32*kb + 8*(v/4) + 4*half + v%4
+  auto mask_max = [&](int tile, f32x16 (&s)[NKB]) {
+    const bool suffix = tile >= nct;
+    const int k0 = suffix ? (tile - nct) * KT : tile * KT;
+    const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
     if (suffix || nvalid < KT) {
 #pragma unroll
       for (int j = 0; j < NKB; ++j)
@@ -734,18 +782,11 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
     for (int j = 0; j < NKB; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s[j][v]);
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float m_ref = (m_new == kNegInf) ? 0.f : m_new;
-    float psum = 0.f;
-#pragma unroll
-    for (int j = 0; j < NKB; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(s[j][v] - m_ref);
-        s[j][v] = p;
-        psum += p;
-      }
+    return fmaxf(m_run, half_pair_max(mt));
+  };
+
+  // ---- rescale the running sum and output to a new maximum
+  auto rescale = [&](float m_new, float m_ref) {
     if (__any(m_new > m_run)) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
       l_run *= alpha;
@@ -754,38 +795,107 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) o[db][v] *= alpha;
     }
-    l_run += psum;
     m_run = m_new;
+  };
 
-    // ---- O^T += V^T P^T.  Chunk c takes accumulator values
-    // v = KPL*(c % CPB) + e of block c / CPB; the matching key is read from sV.
+  // ---- bf16: probabilities packed as P*V operands.  Chunk cc holds values
+  // v0 + e, v0 = 8*(cc % 2), of block cc / 2; its row sum is taken from the
+  // rounded values P*V uses
+  constexpr int NPW = NPC / KG;           // P*V chunks per wavefront and tile
+  auto exp_pack = [&](f32x16 (&s)[NKB], float m_ref, Op (&pb)[NPW]) {
+    float psum = 0.f;
+    if constexpr (KPL == 8) {
+      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+      const bf16x2 ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
 #pragma unroll
-    for (int cc = 0; cc < NPC / KG; ++cc) {
-      const int c = kh * (NPC / KG) + cc;
-      const int j = cc / CPB;
-      const int kb = c / CPB;
-      const int v0 = KPL * (c % CPB);
-      Op pb;
-      if constexpr (KPL == 1) {
-        pb = s[j][v0];
-      } else {
+      for (int cc = 0; cc < NPW; ++cc) {
+        const int j = cc / CPB, v0 = KPL * (cc % CPB);
 #pragma unroll
-        for (int e = 0; e < KPL; ++e) pb[e] = from_f<T>(s[j][v0 + e]);
-      }
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const T* vrow = sV + (db * 32 + qi) * L::LDV + kb * 32 + 4 * half;
-        Op va;
-        if constexpr (KPL == 1) {
-          va = vrow[8 * (v0 >> 2) + (v0 & 3)];
-        } else {
-          // v0 = 8*(c%2): keys 16*(c%2) + 4*half + {0..3} and + 8 + {0..3}
-          const int kofs = 8 * (v0 >> 2);
-          const uint2 lo = *reinterpret_cast<const uint2*>(vrow + kofs);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + kofs + 8);
-          va = __builtin_bit_cast(Op, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        for (int e = 0; e < KPL; e += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(s[j][v0 + e] - m_ref);
+          const float p1 = __builtin_amdgcn_exp2f(s[j][v0 + e + 1] - m_ref);
+          const bf16x2 pp = {static_cast<__bf16>(p0), static_cast<__bf16>(p1)};
+          pb[cc][e] = pp[0];
+          pb[cc][e + 1] = pp[1];
+          psum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, psum, false);
         }
-        o[db] = M::run(va, pb, o[db]);
+      }
+    }
+    return psum;
+  };
+  // ---- O^T += V^T P^T; chunk c of the tile covers keys 16*(c%2) + 4*half +
+  // {0..3} and + 8 + {0..3} of block c / 2
+  auto pv = [&](const T* sV, const Op (&pb)[NPW]) {
+    if constexpr (KPL == 8) {
+#pragma unroll
+      for (int cc = 0; cc < NPW; ++cc) {
+        const int c = kh * NPW + cc;
+        const int kb = c / CPB;
+        const int kofs = 16 * (c % CPB);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const T* vrow = sV + (db * 32 + qi) * L::LDV + kb * 32 + 4 * half + kofs;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
+          o[db] = M::run(__builtin_bit_cast(Op, make_uint4(lo.x, lo.y, hi.x, hi.y)), pb[cc],
+                         o[db]);
+        }
+      }
+    }
+  };
+
+  // prologue: tile t0 (loads issued above) into stage 0, tile t0 + 1 in registers
+  if (t0 + 1 < t1) fetch_idx(t0 + 1);
+  commit(t0, kst(0), vst(0));
+  if (t0 + 1 < t1) fetch_data(t0 + 1);
+  if (t0 + 2 < t1) fetch_idx(t0 + 2);
+  __syncthreads();
+
+  for (int tile = t0; tile < t1; ++tile) {
+    const int stage = (tile - t0) & 1;
+    // next tile into the other stage; its readers finished before the last barrier
+    if (tile + 1 < t1) {
+      commit(tile + 1, kst(stage ^ 1), vst(stage ^ 1));
+      if (tile + 2 < t1) fetch_data(tile + 2);
+      if (tile + 3 < t1) fetch_idx(tile + 3);
+    }
+    f32x16 s[NKB];
+    qk(kst(stage), s);
+    const float m_new = mask_max(tile, s);
+    const float m_ref = (m_new == kNegInf) ? 0.f : m_new;
+    if constexpr (KPL == 8) {
+      // bf16: the same arithmetic as the pipelined loop
+      rescale(m_new, m_ref);
+      Op pb[NPW];
+      l_run += exp_pack(s, m_ref, pb);
+      pv(vst(stage), pb);
+    } else {
+      float psum = 0.f;
+#pragma unroll
+      for (int j = 0; j < NKB; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float p = __builtin_amdgcn_exp2f(s[j][v] - m_ref);
+          s[j][v] = p;
+          psum += p;
+        }
+      rescale(m_new, m_ref);
+      l_run += psum;
+
+      // ---- O^T += V^T P^T with fp32 MFMA: chunk c takes accumulator value
+      // v0 = c % CPB of block c / CPB (key 8*(v0/4) + 4*half + v0%4 of it)
+      const T* sV = vst(stage);
+#pragma unroll
+      for (int cc = 0; cc < NPC / KG; ++cc) {
+        const int c = kh * (NPC / KG) + cc;
+        const int j = cc / CPB;
+        const int kb = c / CPB;
+        const int v0 = KPL * (c % CPB);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const T* vrow = sV + (db * 32 + qi) * L::LDV + kb * 32 + 4 * half;
+          o[db] = M::run(vrow[8 * (v0 >> 2) + (v0 & 3)], s[j][v0], o[db]);
+        }
       }
     }
     __syncthreads();   // next stage written; this stage free for the tile after next
@@ -794,7 +904,7 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
   // ---- the two key halves of a row group combine (same lane, same rows)
   if constexpr (KG == 2) {
     constexpr int XW = 2 + NDB * 16;                     // m, l and this lane's outputs
-    static_assert(NRG * 64 * XW * sizeof(float) <= 2 * L::TILE * sizeof(T),
+    static_assert(NRG * 64 * XW * sizeof(float) <= SBUF * sizeof(T),
                   "key-half exchange must fit in the tile stages");
     float* xs = reinterpret_cast<float*>(sbuf);          // [NRG][64 lanes][XW] floats
     float* mine = xs + (size_t(rgrp) * 64 + lane) * XW;
@@ -822,42 +932,57 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
   }
   const bool writer = KG == 1 || kh == 0;
 
-  // ---- epilogue: accumulator value v of block db holds d = 32*db + 8*(v/4) + 4*half + v%4
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  // ---- epilogue: rows normalised and staged in LDS (accumulator value v of
+  // block db holds d = 32*db + 8*(v/4) + 4*half + v%4), then copied out as
+  // whole rows: to the output, or in the activation dtype to the partials
+  const float l_tot = half_pair_sum(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float lse_val = l_tot > 0.f ? (m_run + __builtin_amdgcn_logf(l_tot)) * kLn2 : kNegInf;
-  if (row_ok && writer) {
-    if (it.partial < 0) {
-      T* orow = static_cast<T*>(a.out) + ((size_t(b) * S + t) * a.Hq + h) * D;
+  constexpr int LDO = D + (sizeof(T) == 2 ? 4 : 2);   // staged row, 8-byte aligned
+  static_assert(NRG * 32 * LDO <= SBUF, "staged rows must fit in the tile stages");
+  if constexpr (KG == 2) __syncthreads();   // the key-half exchange is read before reuse
+  if (writer) {
+    T* srow = sbuf + (rgrp * 32 + qi) * LDO;
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
+    for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int d = 32 * db + 8 * i + 4 * half;
-          if constexpr (sizeof(T) == 4) {
-            *reinterpret_cast<float4*>(orow + d) =
-                make_float4(o[db][4 * i] * inv, o[db][4 * i + 1] * inv,
-                            o[db][4 * i + 2] * inv, o[db][4 * i + 3] * inv);
-          } else {
-            uint2 u;
-            u.x = pack_bf16(o[db][4 * i] * inv, o[db][4 * i + 1] * inv);
-            u.y = pack_bf16(o[db][4 * i + 2] * inv, o[db][4 * i + 3] * inv);
-            *reinterpret_cast<uint2*>(orow + d) = u;
-          }
+      for (int i = 0; i < 4; ++i) {
+        const int d = 32 * db + 8 * i + 4 * half;
+        const float x0 = o[db][4 * i] * inv, x1 = o[db][4 * i + 1] * inv;
+        const float x2 = o[db][4 * i + 2] * inv, x3 = o[db][4 * i + 3] * inv;
+        if constexpr (sizeof(T) == 4) {
+          reinterpret_cast<float2*>(srow + d)[0] = make_float2(x0, x1);
+          reinterpret_cast<float2*>(srow + d)[1] = make_float2(x2, x3);
+        } else {
+          *reinterpret_cast<uint2*>(srow + d) = make_uint2(pack_bf16(x0, x1), pack_bf16(x2, x3));
         }
-      if (a.lse && half == 0) a.lse[(size_t(b) * a.Hq + h) * S + t] = lse_val;
-    } else {
-      float* prow = a.part_o + (size_t(it.partial) * a.RB + rloc) * D;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int d = 32 * db + 8 * i + 4 * half;
-          *reinterpret_cast<float4*>(prow + d) =
-              make_float4(o[db][4 * i] * inv, o[db][4 * i + 1] * inv,
-                          o[db][4 * i + 2] * inv, o[db][4 * i + 3] * inv);
-        }
-      if (half == 0) a.part_lse[size_t(it.partial) * a.RB + rloc] = lse_val;
+      }
+    if (row_ok && half == 0) {
+      if (it.partial < 0) {
+        if (a.lse) a.lse[(size_t(b) * a.Hq + h) * S + t] = lse_val;
+      } else {
+        a.part_lse[size_t(it.partial) * a.RB + rloc] = lse_val;
+      }
+    }
+  }
+  __syncthreads();
+  {
+    constexpr int EPC = 16 / int(sizeof(T));            // elements per 16-byte chunk
+    constexpr int CPR = D / EPC;                         // chunks per row
+    const int nrows = it.nrows;
+    for (int ch = tid; ch < nrows * CPR; ch += NT) {
+      const int rl = ch / CPR, e0 = (ch % CPR) * EPC;
+      const T* src = sbuf + rl * LDO + e0;
+      const uint2 lo = *reinterpret_cast<const uint2*>(src);
+      const uint2 hi = *reinterpret_cast<const uint2*>(src + EPC / 2);
+      T* dst;
+      if (it.partial < 0) {
+        const int r = it.row0 + rl;
+        dst = static_cast<T*>(a.out) + ((size_t(b) * S + r / G) * a.Hq + g * G + r % G) * D + e0;
+      } else {
+        dst = static_cast<T*>(a.part_o) + (size_t(it.partial) * a.RB + rl) * D + e0;
+      }
+      *reinterpret_cast<uint4*>(dst) = make_uint4(lo.x, lo.y, hi.x, hi.y);
     }
   }
 
@@ -1055,7 +1180,7 @@ hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const vo
   ap.v_suf = v_suf;
   ap.out = out;
   ap.lse = lse;
-  ap.part_o = at_mut<float>(ws, p.ws.part_o);
+  ap.part_o = at_mut<unsigned char>(ws, p.ws.part_o);
   ap.part_lse = at_mut<float>(ws, p.ws.part_lse);
   const int n = static_cast<int>(p.items.size());
   const int rows = p.rows_per_block;      // selects the row-block shape
@@ -1078,7 +1203,7 @@ hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st, hi
   mp.S = p.suffix_len;
   mp.RB = p.rows_per_block;
   mp.groups = at<MergeGroup>(p.d_workspace, p.ws.merges);
-  mp.part_o = at<float>(p.d_workspace, p.ws.part_o);
+  mp.part_o = at<unsigned char>(p.d_workspace, p.ws.part_o);
   mp.part_lse = at<float>(p.d_workspace, p.ws.part_lse);
   mp.out = out;
   mp.lse = lse;

@@ -259,7 +259,9 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
                        p.req_slot0[gr.b], p.req_slot0[gr.b + 1] - p.req_slot0[gr.b], 0, 0});
     }
   }
-  p.merge_in_kernel = o.merge_mode == 1 || (o.merge_mode == 0 && p.max_splits <= 8);
+  // the in-kernel merge serialises a row block's combine in one workgroup,
+  // which measured slower than the separate merge kernel at every split count
+  p.merge_in_kernel = o.merge_mode == 1;
 
   // XCD-aware order.  Workgroups are dealt to the 8 XCDs round-robin by index,
   // and each XCD has its own L2.  Items of one (request, kv-head) read the same
@@ -315,7 +317,8 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   w.merges = take(sizeof(MergeGroup) * p.merges.size());
   w.counters = take(sizeof(int32_t) * p.merges.size());
   w.table_bytes = off;
-  w.part_o = take(sizeof(float) * size_t(p.n_partials) * RB * D);
+  const size_t act_bytes = cfg.act_dtype == C2KV_F32 ? 4 : 2;
+  w.part_o = take(act_bytes * size_t(p.n_partials) * RB * D);
   w.part_lse = take(sizeof(float) * size_t(p.n_partials) * RB);
   w.total = off;
 

@@ -44,7 +44,7 @@ struct WorkspaceLayout {
   size_t merges = 0;      // MergeGroup [n_merge]
   size_t counters = 0;    // int32 [n_merge], zero between launches
   size_t table_bytes = 0; // end of the tables (uploaded image size)
-  size_t part_o = 0;      // float [n_partials][rows_per_block][D]
+  size_t part_o = 0;      // activation dtype [n_partials][rows_per_block][D]
   size_t part_lse = 0;    // float [n_partials][rows_per_block]
   size_t total = 0;
 };
