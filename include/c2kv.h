@@ -111,9 +111,10 @@ typedef struct c2kv_plan_opts {
   int32_t kv_splits;       /* > 0: key splits per row block (default: automatic)   */
   int32_t rows_per_block;  /* 128 or 256 query rows per workgroup (automatic)      */
   int32_t num_cus;         /* compute units to size the work list for (256)       */
-  int32_t merge_mode;      /* combining key splits: 0 automatic, 1 the last split
-                              of a row block merges inside the attention kernel,
-                              2 a separate merge kernel                           */
+  int32_t merge_mode;      /* combining key splits: 0 automatic (currently the
+                              separate kernel), 1 the last split of a row block
+                              merges inside the attention kernel, 2 a separate
+                              merge kernel                                        */
 } c2kv_plan_opts;
 
 /* The stored caches KV_reuse (Section 2.2, Eq. 2): device memory, caller-owned. */

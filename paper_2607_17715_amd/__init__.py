@@ -188,8 +188,9 @@ class Plan:
 
     def __del__(self):
         h = getattr(self, "_h", None)
-        if h is not None and h.value:
-            _lib.c2kv_plan_destroy(h)
+        lib_ = _lib
+        if h is not None and h.value and lib_ is not None:   # None at interpreter teardown
+            lib_.c2kv_plan_destroy(h)
             self._h = None
 
     @property

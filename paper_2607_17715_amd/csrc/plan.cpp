@@ -239,7 +239,12 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
         total_tiles += nct + nst;
       }
   }
-  const int64_t per_item = std::max<int64_t>(2, (total_tiles + target - 1) / target);
+  // Key splits only add parallelism where the row blocks alone leave CUs idle;
+  // with at least one row block per CU they would only add partials, a merge
+  // and a second round of workgroups.
+  const bool split = int64_t(groups.size()) < target;
+  const int64_t per_item =
+      split ? std::max<int64_t>(2, (total_tiles + target - 1) / target) : INT32_MAX;
   std::vector<WorkItem> items;
   for (const Group& gr : groups) {
     int32_t ns = o.kv_splits > 0 ? o.kv_splits : ceil_div(gr.tiles, per_item);
