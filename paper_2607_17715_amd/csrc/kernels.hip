@@ -745,18 +745,44 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
 
   // ---- S^T = K Q^T over this wavefront's 32-key blocks, accumulator lane = query
   auto qk = [&](const T* sK, f32x16 (&s)[NKB]) {
+    if constexpr (KPL == 8 && kPaged) {
+      // bf16 from pages: a ring of AH key fragments kept in flight ahead of
+      // their MFMAs, the scheduling fences holding this issue order (measured a
+      // little faster there, a little slower where the loader does more work)
+      constexpr int NF = NKB * NQC, AH = 4;
+      auto frag = [&](int f) {
+        const int kb = kh * NKB + f / NQC;
+        return *reinterpret_cast<const Op*>(sK + (kb * 32 + qi) * L::LDK + half * KPL +
+                                            (f % NQC) * KSTEP);
+      };
+      Op kf[AH];
 #pragma unroll
-    for (int j = 0; j < NKB; ++j) {
-      const int kb = kh * NKB + j;
+      for (int f = 0; f < AH; ++f) kf[f] = frag(f);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) s[j][v] = 0.f;
-      const T* krow = sK + (kb * 32 + qi) * L::LDK + half * KPL;
+      for (int j = 0; j < NKB; ++j)
 #pragma unroll
-      for (int c = 0; c < NQC; ++c) {
-        Op ka;
-        if constexpr (KPL == 1) ka = krow[c * KSTEP];
-        else ka = *reinterpret_cast<const Op*>(krow + c * KSTEP);
-        s[j] = M::run(ka, qop[c], s[j]);
+        for (int v = 0; v < 16; ++v) s[j][v] = 0.f;
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        s[f / NQC] = M::run(kf[f % AH], qop[f % NQC], s[f / NQC]);
+        if (f + AH < NF) kf[f % AH] = frag(f + AH);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NKB; ++j) {
+        const int kb = kh * NKB + j;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) s[j][v] = 0.f;
+        const T* krow = sK + (kb * 32 + qi) * L::LDK + half * KPL;
+#pragma unroll
+        for (int c = 0; c < NQC; ++c) {
+          Op ka;
+          if constexpr (KPL == 1) ka = krow[c * KSTEP];
+          else ka = *reinterpret_cast<const Op*>(krow + c * KSTEP);
+          s[j] = M::run(ka, qop[c], s[j]);
+        }
       }
     }
   };
@@ -826,7 +852,28 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
   // ---- O^T += V^T P^T; chunk c of the tile covers keys 16*(c%2) + 4*half +
   // {0..3} and + 8 + {0..3} of block c / 2
   auto pv = [&](const T* sV, const Op (&pb)[NPW]) {
-    if constexpr (KPL == 8) {
+    if constexpr (KPL == 8 && kPaged) {
+      // value fragments in a ring of AH ahead of their MFMAs, as for the keys
+      constexpr int NF = NPW * NDB, AH = 4;
+      auto frag = [&](int f) {
+        const int cc = f / NDB, db = f % NDB;
+        const int c = kh * NPW + cc;
+        const T* vrow = sV + (db * 32 + qi) * L::LDV + (c / CPB) * 32 + 4 * half + 16 * (c % CPB);
+        const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
+        return __builtin_bit_cast(Op, make_uint4(lo.x, lo.y, hi.x, hi.y));
+      };
+      Op vf[AH];
+#pragma unroll
+      for (int f = 0; f < AH; ++f) vf[f] = frag(f);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        o[f % NDB] = M::run(vf[f % AH], pb[f / NDB], o[f % NDB]);
+        if (f + AH < NF) vf[f % AH] = frag(f + AH);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else if constexpr (KPL == 8) {
 #pragma unroll
       for (int cc = 0; cc < NPW; ++cc) {
         const int c = kh * NPW + cc;
