@@ -44,9 +44,16 @@ WORKLOADS = {
     "ragged-batch-bf16": 3,
     "int8-32layer": 4,
     "70b-long-suffix-bf16": 5,
+    "decode-32k-4x-bf16": 6,
+    "decode-128k-4x-bf16": 7,
+    "decode-128k-16x-bf16": 8,
+    "decode-128k-1x-bf16": 9,
 }
 DEFAULT_WORKLOAD = "llama3-8b-layer-bf16"
 LONG_SUFFIX = {"70b-long-suffix-bf16"}
+# one generated token over a cache composed once beforehand: the step is c2kv_attend
+DECODE = {"decode-32k-4x-bf16", "decode-128k-4x-bf16", "decode-128k-16x-bf16",
+          "decode-128k-1x-bf16"}
 
 
 def log(msg):
@@ -117,7 +124,7 @@ def cpu_baseline(w, idx: int):
                                 w.seg_kept_off, w.kept_idx, w.seg_new_pos0)
     N = int(lay["composed_len"].sum())
     S = w.suffix_len
-    if idx in (1, 2, 4):
+    if idx in (1, 2, 4) or idx >= 6:
         # whole layer, repeated for about 10 s
         reps, t0 = 0, time.perf_counter()
         while True:
@@ -190,6 +197,8 @@ def main():
     composed, span_end = plan.requests()
     work = algorithmic_work(w, composed)
     long_suffix = args.workload in LONG_SUFFIX
+    decode = args.workload in DECODE
+    paged = long_suffix or decode
     act = torch.float32 if w.act_dtype == "f32" else torch.bfloat16
 
     # ---- device inputs, replicated so the rotation spans > 2x the Infinity Cache
@@ -198,24 +207,42 @@ def main():
                 vs=None if w.pool_v_scale is None else c2kv.to_device(w.pool_v_scale, "f32"),
                 q=c2kv.to_device(w.q, w.act_dtype), k_suf=c2kv.to_device(w.k_suf, w.act_dtype),
                 v_suf=c2kv.to_device(w.v_suf, w.act_dtype))
-    footprint = sum(t.numel() * t.element_size() for t in base.values() if t is not None)
+    if paged:
+        ksh, vsh = c2kv.page_shapes(plan)
+    if decode:
+        # the step reads the composed pages; each copy gets its own
+        footprint = 2 * math.prod(ksh) * (4 if act == torch.float32 else 2)
+    else:
+        footprint = sum(t.numel() * t.element_size() for t in base.values() if t is not None)
     copies = args.copies or int(min(64, max(2, math.ceil(2.2 * MALL_BYTES / footprint))))
     log(f"footprint {footprint / 1e6:.1f} MB per copy, {copies} copies")
-    sets = [base] + [{k: (None if t is None else t.clone()) for k, t in base.items()}
-                     for _ in range(copies - 1)]
+    if decode:
+        sets = [dict(base) for _ in range(copies)]          # pool shared: composed once per copy
+    else:
+        sets = [base] + [{k: (None if t is None else t.clone()) for k, t in base.items()}
+                         for _ in range(copies - 1)]
     for s in sets:
         s["pool"] = c2kv.pool_desc(s["k"], s["v"], s["ks"], s["vs"])
         s["out"] = torch.empty_like(s["q"])
         s["lse"] = torch.empty((w.batch, w.n_q_heads, w.suffix_len), dtype=torch.float32,
                                device="cuda")
     if long_suffix:
-        ksh, vsh = c2kv.page_shapes(plan)
         kp = torch.empty(ksh, dtype=act, device="cuda")
         vp = torch.empty(vsh, dtype=act, device="cuda")
+    if decode:
+        for s in sets:
+            s["kp"] = torch.empty(ksh, dtype=act, device="cuda")
+            s["vp"] = torch.empty(vsh, dtype=act, device="cuda")
+            c2kv.c2kv_compose(plan, s["pool"], s["kp"], s["vp"])
+        torch.cuda.synchronize()
+        log(f"composed {copies} page copies (untimed, as at prefill)")
 
     def step(i):
         s = sets[i % copies]
-        if long_suffix:
+        if decode:
+            c2kv.c2kv_attend(plan, s["kp"], s["vp"], s["q"], s["k_suf"], s["v_suf"], s["out"],
+                             s["lse"])
+        elif long_suffix:
             c2kv.c2kv_compose(plan, s["pool"], kp, vp)
             c2kv.c2kv_attend(plan, kp, vp, s["q"], s["k_suf"], s["v_suf"], s["out"], s["lse"])
         else:
@@ -290,7 +317,7 @@ def main():
             kern[name] = {"avg_us": 1e3 * ms / n, "launches": n}
     c2kv.timing_reset()
 
-    dom = "attn_paged" if long_suffix else "attn_pool"
+    dom = "attn_paged" if paged else "attn_pool"
     dom_s = kern[dom]["avg_us"] * 1e-6
     mfma_bound = idx in (3, 5)
     if mfma_bound:
@@ -300,7 +327,7 @@ def main():
                 "frac": achieved / peak}
         dom_bytes = paged_attend_bytes(w, composed) if long_suffix else work["bytes"]
     else:
-        dom_bytes = work["bytes"]
+        dom_bytes = paged_attend_bytes(w, composed) if decode else work["bytes"]
         achieved = dom_bytes / dom_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": achieved / PEAK_HBM_GBS}
@@ -327,7 +354,8 @@ def main():
                    "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
                    "pool_dtype": w.pool_dtype, "batch": w.batch, "suffix_len": w.suffix_len,
                    "composed_tokens": work["tokens"],
-                   "path": "compose+attend" if long_suffix else "compose_attend",
+                   "path": ("attend over composed pages" if decode else
+                            "compose+attend" if long_suffix else "compose_attend"),
                    "plan": {**{k: plan.info[k] for k in ("rows_per_block", "n_work_items",
                                                          "n_merge_groups", "max_splits")},
                             "merge_mode": args.merge_mode},

@@ -1056,15 +1056,94 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
 // merge of key splits as its own kernel (row blocks with many splits)
 // ----------------------------------------------------------------------------
 
+// Rows of one merge group, RPW per workgroup, TPR threads per row with EPT
+// output elements each.  Two dependent memory steps: the split LSEs (reduced
+// across the row's threads into per-split weights in LDS), then the partial
+// rows of up to 16 splits at a time, all loads of a batch in flight together.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
-  constexpr int RPW = 256 / (D / 4);          // rows per workgroup
+  constexpr int EPT = 4;
+  constexpr int TPR = D / EPT;                 // threads per row
+  constexpr int RPW = 256 / TPR;               // rows per workgroup
+  constexpr int NPS = kMaxSplits / TPR;        // split LSEs per thread
+  __shared__ float s_w[kMaxSplits][RPW];
   const MergeGroup mg = a.groups[blockIdx.x];
   const int rlo = blockIdx.y * RPW;
-  const int rhi = min(rlo + RPW, mg.nrows);
-  if (rlo >= rhi) return;
-  merge_rows<T, D>(mg, rlo, rhi, a.part_o, a.part_lse, a.RB, a.Hq, a.G, a.S, a.out, a.lse,
-                   threadIdx.x, 256);
+  if (rlo >= mg.nrows) return;
+  const int tid = threadIdx.x, rl = tid / TPR, sub = tid % TPR;
+  const int rloc = rlo + rl;
+  const bool ok = rloc < mg.nrows;
+  const float* pl = a.part_lse + size_t(mg.part0) * a.RB + rloc;
+
+  // Loads are unconditional, from indices clamped into the group's partials
+  // (rows of a partial exist up to RB), so that no load waits at a branch join;
+  // what lies past the row count or the split count gets weight zero.
+  const int last = mg.nsplit - 1;
+  float li[NPS];
+#pragma unroll
+  for (int k = 0; k < NPS; ++k) li[k] = pl[size_t(min(sub + k * TPR, last)) * a.RB];
+  float mx = kNegInf;
+#pragma unroll
+  for (int k = 0; k < NPS; ++k) {
+    if (!ok || sub + k * TPR > last) li[k] = kNegInf;
+    mx = fmaxf(mx, li[k]);
+  }
+#pragma unroll
+  for (int off = 1; off < TPR; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  float z = 0.f;
+#pragma unroll
+  for (int k = 0; k < NPS; ++k) {
+    const int i = sub + k * TPR;
+    const float e = (li[k] == kNegInf) ? 0.f : __expf(li[k] - mx);
+    if (i < mg.nsplit) s_w[i][rl] = e;
+    z += e;
+  }
+#pragma unroll
+  for (int off = 1; off < TPR; off <<= 1) z += __shfl_xor(z, off);
+  __syncthreads();
+
+  float acc[EPT] = {};
+  const T* po = static_cast<const T*>(a.part_o) + (size_t(mg.part0) * a.RB + rloc) * D + sub * EPT;
+  for (int i0 = 0; i0 < mg.nsplit; i0 += 16) {
+    float v[16][EPT];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      {
+        const T* src = po + size_t(min(i0 + k, last)) * a.RB * D;
+        if constexpr (sizeof(T) == 4) {
+          const float4 x = *reinterpret_cast<const float4*>(src);
+          v[k][0] = x.x; v[k][1] = x.y; v[k][2] = x.z; v[k][3] = x.w;
+        } else {
+          const uint2 u = *reinterpret_cast<const uint2*>(src);
+          v[k][0] = __uint_as_float(u.x << 16);
+          v[k][1] = __uint_as_float(u.x & 0xffff0000u);
+          v[k][2] = __uint_as_float(u.y << 16);
+          v[k][3] = __uint_as_float(u.y & 0xffff0000u);
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int i = i0 + k;
+      const float w = s_w[min(i, last)][rl] * (i <= last ? 1.f : 0.f);
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) acc[e] += w * v[k][e];
+    }
+  }
+  if (!ok) return;
+  const float inv = z > 0.f ? 1.f / z : 0.f;
+  const int r = mg.row0 + rloc;
+  const int t = r / a.G, h = mg.g * a.G + r % a.G;
+  T* orow = static_cast<T*>(a.out) + ((size_t(mg.b) * a.S + t) * a.Hq + h) * D + sub * EPT;
+  if constexpr (sizeof(T) == 4) {
+    *reinterpret_cast<float4*>(orow) =
+        make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+  } else {
+    *reinterpret_cast<uint2*>(orow) =
+        make_uint2(pack_bf16(acc[0] * inv, acc[1] * inv), pack_bf16(acc[2] * inv, acc[3] * inv));
+  }
+  if (a.lse && sub == 0)
+    a.lse[(size_t(mg.b) * a.Hq + h) * a.S + t] = z > 0.f ? mx + __logf(z) : kNegInf;
 }
 
 // ----------------------------------------------------------------------------

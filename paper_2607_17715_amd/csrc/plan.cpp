@@ -248,7 +248,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   std::vector<WorkItem> items;
   for (const Group& gr : groups) {
     int32_t ns = o.kv_splits > 0 ? o.kv_splits : ceil_div(gr.tiles, per_item);
-    ns = std::max(1, std::min(ns, gr.tiles));
+    ns = std::max(1, std::min({ns, gr.tiles, kMaxSplits}));
     p.max_splits = std::max(p.max_splits, ns);
     int32_t part0 = -1, merge = -1;
     if (ns > 1) {

@@ -14,6 +14,7 @@
 namespace c2kv {
 
 constexpr int kKeyTile = 64;        // keys per attention / compose tile
+constexpr int kMaxSplits = 256;     // key splits of one row block (merge kernel's LDS table)
 constexpr int kRowsPerWave = 32;    // query rows one wavefront owns (MFMA 32-wide)
 
 // One attention workgroup: query rows [row0, row0 + nrows) of (request b,

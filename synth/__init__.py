@@ -148,7 +148,8 @@ class Spec:
 
 
 def spec(idx: int) -> Spec:
-    """The five synthetic workloads (1-based index)."""
+    """The synthetic workloads (1-based index): five prefill-style layers, then
+    four decode steps."""
     if idx == 1:   # tiny fp32
         return Spec("tiny-fp32", 8, 2, 64, 1e4, "f32", "f32", 4, 256, 16, 1, 4,
                     "natural", ("count", 128), 32)
@@ -164,6 +165,20 @@ def spec(idx: int) -> Spec:
     if idx == 5:   # 70B-shaped long suffix
         return Spec("70b-long-suffix-bf16", 64, 8, 128, 5e5, "bf16", "bf16", 32, 2048, 0,
                     1, 32, "natural", ("count", 1024), 2048)
+    # decode steps (one new token) over a composed context of 2048-token chunks
+    # with 4x / 16x compression or none, Llama-3-8B shapes
+    if idx == 6:
+        return Spec("decode-32k-4x-bf16", 32, 8, 128, 5e5, "bf16", "bf16", 16, 2048, 0,
+                    1, 16, "natural", ("count", 512), 1)
+    if idx == 7:
+        return Spec("decode-128k-4x-bf16", 32, 8, 128, 5e5, "bf16", "bf16", 64, 2048, 0,
+                    1, 64, "natural", ("count", 512), 1)
+    if idx == 8:
+        return Spec("decode-128k-16x-bf16", 32, 8, 128, 5e5, "bf16", "bf16", 64, 2048, 0,
+                    1, 64, "natural", ("count", 128), 1)
+    if idx == 9:
+        return Spec("decode-128k-1x-bf16", 32, 8, 128, 5e5, "bf16", "bf16", 64, 2048, 0,
+                    1, 64, "natural", ("all",), 1)
     raise ValueError(idx)
 
 

@@ -59,6 +59,25 @@ def test_long_suffix_sampled_rows():
 
 
 # ---------------------------------------------------------------------------
+# decode steps: one suffix token over the composed cache (split-K over keys)
+# ---------------------------------------------------------------------------
+
+def test_decode_small():
+    sp = synth.Spec("decode-small", 32, 8, 128, 5e5, "bf16", "bf16", 8, 512, 0, 1, 8,
+                    "natural", ("count", 128), 1)
+    _both_paths(synth.build(sp, seed=11), "decode-small")
+
+
+def test_decode_32k_4x():
+    _both_paths(synth.config(6), "decode-32k-4x")
+
+
+def test_decode_128k_4x():
+    """The 128k-context decode with 4x compression at full size."""
+    _both_paths(synth.config(7), "decode-128k-4x")
+
+
+# ---------------------------------------------------------------------------
 # compose: layout bit-exact, values, delta = 0 copies
 # ---------------------------------------------------------------------------
 
