@@ -48,6 +48,8 @@ WORKLOADS = {
     "decode-128k-4x-bf16": 7,
     "decode-128k-16x-bf16": 8,
     "decode-128k-1x-bf16": 9,
+    "llama3-8b-layer-prerope-bf16": 10,
+    "llama3-8b-layer-c2x4-bf16": 11,
 }
 DEFAULT_WORKLOAD = "llama3-8b-layer-bf16"
 LONG_SUFFIX = {"70b-long-suffix-bf16"}
@@ -124,7 +126,7 @@ def cpu_baseline(w, idx: int):
                                 w.seg_kept_off, w.kept_idx, w.seg_new_pos0)
     N = int(lay["composed_len"].sum())
     S = w.suffix_len
-    if idx in (1, 2, 4) or idx >= 6:
+    if idx in (1, 2, 4) or idx >= 6:   # every workload but the two largest prefills
         # whole layer, repeated for about 10 s
         reps, t0 = 0, time.perf_counter()
         while True:

@@ -90,6 +90,17 @@ typedef struct c2kv_attn_cfg {
 
 /* The composition B(x_s, KV_1..KV_K) of a batch of requests (Section 2.2, Eq. 3;
  * Section 3.2).  HOST arrays, read only inside c2kv_plan_create. */
+/* How the pool stores its keys. */
+typedef enum c2kv_key_encoding {
+  C2KV_KEYS_ROPE_AT_ORIG = 0,   /* RoPE-encoded at seg_orig_pos0 + j; composing turns each
+                                   key by delta = new_pos0 - orig_pos0 (Section 3.2
+                                   "Output and Reuse", Appendix C)                        */
+  C2KV_KEYS_PRE_ROPE = 1        /* stored before positional encoding (Section 3.3.1);
+                                   composing encodes each key at its new position
+                                   new_pos0 + j.  The cos/sin table then has one row per
+                                   composed slot instead of one per segment               */
+} c2kv_key_encoding;
+
 typedef struct c2kv_compose_desc {
   int32_t batch;                 /* B >= 1                                          */
   int32_t n_segments;            /* total segments over all requests                */
@@ -103,6 +114,7 @@ typedef struct c2kv_compose_desc {
   const int32_t* seg_kept_off;   /* [n_segments+1] CSR into kept_idx                */
   const int32_t* kept_idx;       /* strictly ascending within a segment, each in
                                     [0, seg_span); a segment may keep nothing       */
+  int32_t key_encoding;          /* c2kv_key_encoding of the pool's keys            */
 } c2kv_compose_desc;
 
 /* Launch-shape options.  Zero fields select the defaults. */

@@ -156,12 +156,14 @@ def compose_layout(req_seg_off, seg_row0, seg_span, seg_orig_pos0, seg_kept_off,
 # ---------------------------------------------------------------------------
 
 def compose(layout: dict, pool_k, pool_v, pool_dtype: str, base: float,
-            k_scale=None, v_scale=None, rerotate: bool = True):
+            k_scale=None, v_scale=None, rerotate: bool = True, pre_rope: bool = False):
     """Composed cache of every request: list of (K [N_r, H_kv, d], V [N_r, H_kv, d]).
 
     Each slot's key is turned by its segment's delta (the same angle for all of
     its kv-heads); values are not rotated.  rerotate=False is the Fixed-Pos
-    ablation (delta taken as 0)."""
+    ablation (delta taken as 0).  pre_rope=True reads the stored keys as taken
+    before positional encoding (Section 3.3.1) and encodes each one at its new
+    position p_new instead."""
     res = []
     for r in range(len(layout["src_row"])):
         rows = layout["src_row"][r]
@@ -170,9 +172,9 @@ def compose(layout: dict, pool_k, pool_v, pool_dtype: str, base: float,
         v = decode_storage(pool_v[rows], pool_dtype,
                            None if v_scale is None else v_scale[rows])
         if rerotate and len(rows):
-            delta = layout["delta"][r].astype(np.float64)[:, None]   # [N, 1] -> per head
-            delta = np.broadcast_to(delta, k.shape[:-1])
-            k = rope_rotate(k, delta, base)
+            turn = layout["p_new" if pre_rope else "delta"][r].astype(np.float64)[:, None]
+            turn = np.broadcast_to(turn, k.shape[:-1])              # the same for every head
+            k = rope_rotate(k, turn, base)
         res.append((k, v))
     return res
 
@@ -239,7 +241,8 @@ def compose_attend(w, rows: Optional[Sequence[int]] = None, requests=None,
     sub = {k: [layout[k][r] for r in reqs] if isinstance(layout[k], list) else layout[k]
            for k in layout}
     caches = compose(sub, w.pool_k, w.pool_v, w.pool_dtype, w.rope_base,
-                     w.pool_k_scale, w.pool_v_scale, rerotate=rerotate)
+                     w.pool_k_scale, w.pool_v_scale, rerotate=rerotate,
+                     pre_rope=getattr(w, "keys_pre_rope", False))
     act = w.act_dtype
     outs, lses = [], []
     for i, r in enumerate(reqs):

@@ -21,6 +21,7 @@ LIB_PATH = os.environ.get("C2KV_LIBRARY") or os.path.join(_PKG, "libc2kv.so")
 C2KV_OK, C2KV_E_INVAL, C2KV_E_UNSUPPORTED, C2KV_E_WORKSPACE, C2KV_E_HIP, C2KV_E_NOMEM, \
     C2KV_E_STATE = 0, -1, -2, -3, -4, -5, -6
 C2KV_F32, C2KV_BF16, C2KV_I8 = 0, 1, 2
+C2KV_KEYS_ROPE_AT_ORIG, C2KV_KEYS_PRE_ROPE = 0, 1
 _DTYPE_CODE = {"f32": C2KV_F32, "bf16": C2KV_BF16, "i8": C2KV_I8}
 
 EXPORTED = [
@@ -48,7 +49,7 @@ class ComposeDesc(ctypes.Structure):
                 ("req_seg_off", ctypes.c_void_p), ("seg_row0", ctypes.c_void_p),
                 ("seg_span", ctypes.c_void_p), ("seg_orig_pos0", ctypes.c_void_p),
                 ("seg_new_pos0", ctypes.c_void_p), ("seg_kept_off", ctypes.c_void_p),
-                ("kept_idx", ctypes.c_void_p)]
+                ("kept_idx", ctypes.c_void_p), ("key_encoding", ctypes.c_int32)]
 
 
 class PlanOpts(ctypes.Structure):
@@ -150,7 +151,8 @@ class Plan:
                  rope_base: float, req_seg_off, seg_row0, seg_span, seg_orig_pos0,
                  seg_kept_off, kept_idx, suffix_len: int, seg_new_pos0=None,
                  softmax_scale: float = 0.0, page_size: int = 0, kv_splits: int = 0,
-                 rows_per_block: int = 0, num_cus: int = 0, merge_mode: int = 0):
+                 rows_per_block: int = 0, num_cus: int = 0, merge_mode: int = 0,
+                 keys_pre_rope: bool = False):
         self._arrays = dict(
             req_seg_off=np.ascontiguousarray(req_seg_off, np.int32),
             seg_row0=np.ascontiguousarray(seg_row0, np.int64),
@@ -168,7 +170,8 @@ class Plan:
                            _np_ptr(a["req_seg_off"]), _np_ptr(a["seg_row0"]),
                            _np_ptr(a["seg_span"]), _np_ptr(a["seg_orig_pos0"]),
                            _np_ptr(a["seg_new_pos0"]), _np_ptr(a["seg_kept_off"]),
-                           _np_ptr(a["kept_idx"]))
+                           _np_ptr(a["kept_idx"]), C2KV_KEYS_PRE_ROPE if keys_pre_rope
+                           else C2KV_KEYS_ROPE_AT_ORIG)
         opts = PlanOpts(page_size, kv_splits, rows_per_block, num_cus, merge_mode)
         h = ctypes.c_void_p()
         _check(_lib.c2kv_plan_create(ctypes.byref(self.cfg), ctypes.byref(desc),
@@ -184,7 +187,8 @@ class Plan:
     def for_workload(cls, w, **opts) -> "Plan":
         return cls(w.n_q_heads, w.n_kv_heads, w.head_dim, w.act_dtype, w.rope_base,
                    w.req_seg_off, w.seg_row0, w.seg_span, w.seg_orig_pos0, w.seg_kept_off,
-                   w.kept_idx, w.suffix_len, seg_new_pos0=w.seg_new_pos0, **opts)
+                   w.kept_idx, w.suffix_len, seg_new_pos0=w.seg_new_pos0,
+                   keys_pre_rope=getattr(w, "keys_pre_rope", False), **opts)
 
     def __del__(self):
         h = getattr(self, "_h", None)

@@ -129,6 +129,11 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   p.page_size = o.page_size;
   p.n_segments = nseg;
   p.group = cfg.n_q_heads / cfg.n_kv_heads;
+  if (d.key_encoding != C2KV_KEYS_ROPE_AT_ORIG && d.key_encoding != C2KV_KEYS_PRE_ROPE) {
+    err = "key_encoding must be C2KV_KEYS_ROPE_AT_ORIG or C2KV_KEYS_PRE_ROPE";
+    return C2KV_E_INVAL;
+  }
+  p.keys_pre_rope = d.key_encoding == C2KV_KEYS_PRE_ROPE;
   p.softmax_scale = cfg.softmax_scale > 0.f ? cfg.softmax_scale
                                             : static_cast<float>(1.0 / std::sqrt(double(cfg.head_dim)));
   p.qscale_log2 = static_cast<float>(double(p.softmax_scale) * 1.4426950408889634);
@@ -314,7 +319,10 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   w.req_slot0 = take(sizeof(int32_t) * (B + 1));
   w.slot_info = take(sizeof(int32_t) * 2 * total);
   w.slot_pos = take(sizeof(int32_t) * total);
-  w.seg_cs = take(sizeof(float) * 2 * size_t(std::max(nseg, 1)) * H);
+  // one cos/sin row per segment (angle delta * theta_i), or per slot for keys
+  // stored before RoPE (angle p_new * theta_i); slot_info's second field is the row
+  const int64_t cs_rows = p.keys_pre_rope ? total : nseg;
+  w.seg_cs = take(sizeof(float) * 2 * size_t(std::max<int64_t>(cs_rows, 1)) * H);
   w.suf_cs = take(sizeof(float) * 2 * size_t(B) * S * H);
   w.block_table = take(sizeof(int32_t) * p.block_table.size());
   w.compose_tiles = take(sizeof(int32_t) * p.compose_tiles.size());
@@ -336,7 +344,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
     int32_t* si = reinterpret_cast<int32_t*>(p.image.data() + w.slot_info);
     for (int64_t i = 0; i < total; ++i) {
       si[2 * i] = p.slot_src[i];
-      si[2 * i + 1] = p.slot_seg[i];
+      si[2 * i + 1] = p.keys_pre_rope ? static_cast<int32_t>(i) : p.slot_seg[i];
     }
   }
   put(w.slot_pos, p.slot_pos.data(), sizeof(int32_t) * total);
@@ -348,12 +356,14 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   // cos/sin tables: angles in float64, rounded once to float32
   const std::vector<double> theta = rope_theta(D, cfg.rope_base);
   float* seg_cs = reinterpret_cast<float*>(p.image.data() + w.seg_cs);
-  for (int c = 0; c < nseg; ++c)
+  for (int64_t c = 0; c < cs_rows; ++c) {
+    const double turn = p.keys_pre_rope ? double(p.slot_pos[c]) : double(p.seg_delta[c]);
     for (int i = 0; i < H; ++i) {
-      const double ang = double(p.seg_delta[c]) * theta[i];
+      const double ang = turn * theta[i];
       seg_cs[(size_t(c) * H + i) * 2 + 0] = static_cast<float>(std::cos(ang));
       seg_cs[(size_t(c) * H + i) * 2 + 1] = static_cast<float>(std::sin(ang));
     }
+  }
   float* suf_cs = reinterpret_cast<float*>(p.image.data() + w.suf_cs);
   for (int b = 0; b < B; ++b)
     for (int64_t t = 0; t < S; ++t)

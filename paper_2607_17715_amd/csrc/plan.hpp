@@ -54,6 +54,7 @@ struct Plan {
   c2kv_attn_cfg cfg{};
   int32_t batch = 0, suffix_len = 0, page_size = 64, n_segments = 0;
   int32_t group = 1;               // G = H_q / H_kv
+  bool keys_pre_rope = false;      // pool keys stored before RoPE: per-slot cos/sin rows
   float qscale_log2 = 0.f;         // softmax scale * log2(e)
   float softmax_scale = 0.f;
 

@@ -116,6 +116,7 @@ class Workload:
     q: np.ndarray
     k_suf: np.ndarray
     v_suf: np.ndarray
+    keys_pre_rope: bool = False  # pool keys taken as stored before RoPE (same values)
 
     @property
     def batch(self) -> int:
@@ -145,6 +146,7 @@ class Spec:
     keep: tuple                  # ('count', m) | ('ratio', lo, hi) | ('c2', k) | ('all',)
     suffix_len: int
     layers: int = 1
+    keys_pre_rope: bool = False
 
 
 def spec(idx: int) -> Spec:
@@ -179,6 +181,14 @@ def spec(idx: int) -> Spec:
     if idx == 9:
         return Spec("decode-128k-1x-bf16", 32, 8, 128, 5e5, "bf16", "bf16", 64, 2048, 0,
                     1, 64, "natural", ("all",), 1)
+    # the Llama-3-8B layer with keys stored before RoPE, and with C^2-pattern kept
+    # sets (block ends at compression 4)
+    if idx == 10:
+        return Spec("llama3-8b-layer-prerope-bf16", 32, 8, 128, 5e5, "bf16", "bf16", 8, 512,
+                    64, 1, 8, "shuffled", ("count", 128), 64, keys_pre_rope=True)
+    if idx == 11:
+        return Spec("llama3-8b-layer-c2x4-bf16", 32, 8, 128, 5e5, "bf16", "bf16", 8, 512, 64,
+                    1, 8, "shuffled", ("c2", 4), 64)
     raise ValueError(idx)
 
 
@@ -272,7 +282,7 @@ def build(sp: Spec, layer: int = 0, seed: Optional[int] = None) -> Workload:
         seg_orig_pos0=np.array(seg_orig, np.int32), seg_new_pos0=None,
         seg_kept_off=np.array(kept_off, np.int32),
         kept_idx=(np.concatenate(kept) if kept else np.zeros(0, np.int32)).astype(np.int32),
-        suffix_len=S, q=q, k_suf=k_suf, v_suf=v_suf)
+        suffix_len=S, q=q, k_suf=k_suf, v_suf=v_suf, keys_pre_rope=sp.keys_pre_rope)
 
 
 def config(idx: int, layer: int = 0) -> Workload:

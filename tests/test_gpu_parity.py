@@ -78,6 +78,34 @@ def test_decode_128k_4x():
 
 
 # ---------------------------------------------------------------------------
+# keys stored before RoPE; C^2-pattern kept sets at compression 4 / 8 / 10 / 16
+# ---------------------------------------------------------------------------
+
+def test_llama3_8b_layer_pre_rope_keys():
+    _both_paths(synth.config(10), "llama3-8b-layer-prerope")
+
+
+def test_llama3_8b_layer_c2_pattern():
+    _both_paths(synth.config(11), "llama3-8b-layer-c2x4")
+
+
+@pytest.mark.parametrize("ratio", [4, 8, 10, 16])
+@pytest.mark.parametrize("pre_rope", [False, True])
+def test_c2_pattern_ratios(ratio, pre_rope):
+    w = synth.small(batch=3, keep=("c2", ratio), n_q_heads=16, n_kv_heads=4, suffix_len=40,
+                    chunk_len=300, seed=20 + ratio)
+    w = synth.with_overrides(w, keys_pre_rope=pre_rope)
+    _both_paths(w, f"c2-pattern-x{ratio}-prerope{int(pre_rope)}")
+
+
+@pytest.mark.parametrize("pool_dtype", ["f32", "i8"])
+def test_pre_rope_other_storage(pool_dtype):
+    w = synth.small(pool_dtype=pool_dtype, act_dtype="f32" if pool_dtype == "f32" else "bf16",
+                    batch=2, keep=("ratio", 0.2, 0.6), seed=31)
+    _both_paths(synth.with_overrides(w, keys_pre_rope=True), f"pre-rope-{pool_dtype}")
+
+
+# ---------------------------------------------------------------------------
 # compose: layout bit-exact, values, delta = 0 copies
 # ---------------------------------------------------------------------------
 

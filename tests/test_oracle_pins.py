@@ -240,6 +240,34 @@ def test_rerotation_equals_encoding_at_global_positions(seed):
     np.testing.assert_allclose(out[0], ref, atol=1e-10, rtol=0)
 
 
+@pytest.mark.parametrize("seed,keep", [(7, ("all",)), (8, ("ratio", 0.2, 0.7)),
+                                       (9, ("c2", 4))])
+def test_pre_rope_keys_encoded_at_new_positions(seed, keep):
+    """Keys stored before positional encoding (Section 3.3.1): each kept key is
+    encoded at its new position, checked against the complex form of RoPE and
+    torch's SDPA over [composed keys | suffix]."""
+    w = synth.small(pool_dtype="f32", keep=keep, n_pool_chunks=3, chunk_len=11,
+                    prefix_len=5, batch=1, chunks_per_req=3, suffix_len=6, head_dim=16,
+                    n_q_heads=6, n_kv_heads=2, seed=seed, order="shuffled")
+    w = synth.with_overrides(w, keys_pre_rope=True)
+    base = w.rope_base
+    out, _, lay = oracle.compose_attend(w)
+    rows = lay["src_row"][0]
+    k_glob = _rope_complex(w.pool_k[rows].astype(np.float64),
+                           lay["p_new"][0][:, None].astype(np.float64), base)
+    vc = w.pool_v[rows].astype(np.float64)
+    S = w.suffix_len
+    se = int(lay["span_end"][0])
+    ks = _rope_complex(w.k_suf[0].astype(np.float64), (se + np.arange(S))[:, None], base)
+    qp = _rope_complex(w.q[0].astype(np.float64), (se + np.arange(S))[:, None], base)
+    ref = _sdpa_reference(np.concatenate([k_glob, ks]), np.concatenate([vc, w.v_suf[0]]),
+                          qp, None, len(rows), w.n_q_heads, w.n_kv_heads)
+    np.testing.assert_allclose(out[0], ref, atol=1e-10, rtol=0)
+    # and it is not the delta reading of the same stored values
+    other, _, _ = oracle.compose_attend(synth.with_overrides(w, keys_pre_rope=False))
+    assert np.abs(other - out).max() > 1e-3
+
+
 def test_fixed_pos_ablation_differs():
     """Section 4.8 (Fixed-Pos): without re-rotation the result changes."""
     w = synth.small(pool_dtype="f32", head_dim=16, suffix_len=4, batch=1)

@@ -42,7 +42,7 @@ def _assert_layout_equal(w, plan):
     np.testing.assert_array_equal(dl, np.concatenate(lay["delta"]) if len(dl) else dl)
 
 
-@pytest.mark.parametrize("idx", [1, 2, 4, 5, 6])
+@pytest.mark.parametrize("idx", [1, 2, 4, 5, 6, 10, 11])
 def test_layout_bit_exact_configs(idx):
     w = synth.config(idx)
     _assert_layout_equal(w, c2kv.Plan.for_workload(w))
@@ -130,6 +130,7 @@ def test_validation_errors():
     _expect_status(E.C2KV_E_INVAL, mk(rows_per_block=48))
     _expect_status(E.C2KV_E_INVAL, mk(rows_per_block=64))
     _expect_status(E.C2KV_E_INVAL, mk(merge_mode=3))
+    mk(keys_pre_rope=True)()                                        # the other key encoding
     bad = w.kept_idx.copy()
     bad[0], bad[1] = bad[1], bad[0]
     _expect_status(E.C2KV_E_INVAL, mk(kept_idx=bad))                  # not ascending
@@ -147,6 +148,26 @@ def test_validation_errors():
     row0 = w.seg_row0.copy()
     row0[-1] = 2**31
     _expect_status(E.C2KV_E_UNSUPPORTED, mk(seg_row0=row0))
+
+
+def test_key_encoding_is_validated():
+    w = synth.small(batch=1)
+    a = {k: np.ascontiguousarray(getattr(w, k)) for k in
+         ("req_seg_off", "seg_row0", "seg_span", "seg_orig_pos0", "seg_kept_off", "kept_idx")}
+    cfg = c2kv.AttnCfg(w.n_q_heads, w.n_kv_heads, w.head_dim, c2kv.C2KV_BF16, w.rope_base, 0.0)
+    ptr = lambda x: x.ctypes.data_as(ctypes.c_void_p)
+    for enc, want in ((c2kv.C2KV_KEYS_ROPE_AT_ORIG, c2kv.C2KV_OK),
+                      (c2kv.C2KV_KEYS_PRE_ROPE, c2kv.C2KV_OK), (2, c2kv.C2KV_E_INVAL),
+                      (-1, c2kv.C2KV_E_INVAL)):
+        desc = c2kv.ComposeDesc(w.batch, w.n_segments, ptr(a["req_seg_off"]), ptr(a["seg_row0"]),
+                                ptr(a["seg_span"]), ptr(a["seg_orig_pos0"]), None,
+                                ptr(a["seg_kept_off"]), ptr(a["kept_idx"]), enc)
+        h = ctypes.c_void_p()
+        st = c2kv.lib().c2kv_plan_create(ctypes.byref(cfg), ctypes.byref(desc), w.suffix_len,
+                                         None, ctypes.byref(h))
+        assert st == want, (enc, st)
+        if st == c2kv.C2KV_OK:
+            c2kv.lib().c2kv_plan_destroy(h)
 
 
 def test_calls_need_an_uploaded_plan():
