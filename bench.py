@@ -50,12 +50,21 @@ WORKLOADS = {
     "decode-128k-1x-bf16": 9,
     "llama3-8b-layer-prerope-bf16": 10,
     "llama3-8b-layer-c2x4-bf16": 11,
+    "llama3-8b-layer-host-zerocopy": 2,
+    "llama3-8b-layer-host-load": 2,
+    "int8-layer-host-zerocopy": 4,
+    "int8-layer-host-load": 4,
 }
 DEFAULT_WORKLOAD = "llama3-8b-layer-bf16"
 LONG_SUFFIX = {"70b-long-suffix-bf16"}
 # one generated token over a cache composed once beforehand: the step is c2kv_attend
 DECODE = {"decode-32k-4x-bf16", "decode-128k-4x-bf16", "decode-128k-16x-bf16",
           "decode-128k-1x-bf16"}
+# the load step: chunks stored compressed in page-locked host memory, read in place by the
+# fused kernel over the host link, or copied to the device first (c2kv_load)
+HOST_ZEROCOPY = {"llama3-8b-layer-host-zerocopy", "int8-layer-host-zerocopy"}
+HOST_LOAD = {"llama3-8b-layer-host-load", "int8-layer-host-load"}
+PEAK_HOST_LINK_GBS = 64.0       # PCIe 5.0 x16, one direction
 
 
 def log(msg):
@@ -193,6 +202,10 @@ def main():
     idx = WORKLOADS[args.workload]
     log(f"workload {args.workload}: generating inputs")
     w = synth.config(idx)
+    host_mode = ("zerocopy" if args.workload in HOST_ZEROCOPY else
+                 "load" if args.workload in HOST_LOAD else None)
+    if host_mode:
+        w = synth.compress_pool(w)
     plan = c2kv.Plan.for_workload(w, kv_splits=args.kv_splits,
                                   rows_per_block=args.rows_per_block,
                                   merge_mode=args.merge_mode).upload()
@@ -218,7 +231,18 @@ def main():
         footprint = sum(t.numel() * t.element_size() for t in base.values() if t is not None)
     copies = args.copies or int(min(64, max(2, math.ceil(2.2 * MALL_BYTES / footprint))))
     log(f"footprint {footprint / 1e6:.1f} MB per copy, {copies} copies")
-    if decode:
+    if host_mode:
+        # host memory is not cached on the device side: two copies, each with its
+        # own device pool (the load destination)
+        copies = args.copies or 2
+        hosts = [c2kv.HostPool(w.pool_k, w.pool_v, w.pool_dtype, w.pool_k_scale,
+                               w.pool_v_scale) for _ in range(copies)]
+        sets = [base] + [{k: (None if t is None else t.clone()) for k, t in base.items()}
+                         for _ in range(copies - 1)]
+        for s, h in zip(sets, hosts):
+            s["host"] = h.desc
+        log(f"host pools: {copies} x {hosts[0].nbytes / 1e6:.1f} MB page-locked")
+    elif decode:
         sets = [dict(base) for _ in range(copies)]          # pool shared: composed once per copy
     else:
         sets = [base] + [{k: (None if t is None else t.clone()) for k, t in base.items()}
@@ -241,7 +265,14 @@ def main():
 
     def step(i):
         s = sets[i % copies]
-        if decode:
+        if host_mode == "zerocopy":
+            c2kv.c2kv_compose_attend(plan, s["host"], s["q"], s["k_suf"], s["v_suf"], s["out"],
+                                     s["lse"])
+        elif host_mode == "load":
+            c2kv.c2kv_load(plan, s["host"], s["pool"])
+            c2kv.c2kv_compose_attend(plan, s["pool"], s["q"], s["k_suf"], s["v_suf"], s["out"],
+                                     s["lse"])
+        elif decode:
             c2kv.c2kv_attend(plan, s["kp"], s["vp"], s["q"], s["k_suf"], s["v_suf"], s["out"],
                              s["lse"])
         elif long_suffix:
@@ -367,6 +398,14 @@ def main():
         "eager_ms_per_step": eager_ms,
         "source_sha": kernel_source_sha(),
     }
+    if host_mode:
+        link = hosts[0].nbytes                  # every stored row of the compressed chunks
+        result["host_link"] = {"bytes": link, "achieved": link / (ms_per_step * 1e-3) / 1e9,
+                               "peak": PEAK_HOST_LINK_GBS, "unit": "GB/s",
+                               "frac": link / (ms_per_step * 1e-3) / 1e9 / PEAK_HOST_LINK_GBS,
+                               "path": ("kernel reads over the host link" if host_mode == "zerocopy"
+                                        else "copy engines, then the fused kernel")}
+        result["config"]["path"] = result["config"]["path"] + f" (pool in host memory, {host_mode})"
     if not args.no_cpu_baseline:
         log("timing the float64 oracle on the host (cpu_baseline)")
         result["cpu_baseline"] = cpu_baseline(w, idx)

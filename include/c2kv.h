@@ -101,6 +101,16 @@ typedef enum c2kv_key_encoding {
                                    composed slot instead of one per segment               */
 } c2kv_key_encoding;
 
+/* Where a segment's kept tokens sit in the pool. */
+typedef enum c2kv_pool_layout {
+  C2KV_POOL_FULL = 0,         /* chunks stored whole: kept token j of a segment is pool
+                                 row seg_row0 + j                                       */
+  C2KV_POOL_COMPRESSED = 1    /* chunks stored compressed, only their kept tokens, in
+                                 order (Section 3.2: the compressed cache is what is
+                                 saved): the k-th kept token of a segment is pool row
+                                 seg_row0 + k; its position still comes from kept_idx */
+} c2kv_pool_layout;
+
 typedef struct c2kv_compose_desc {
   int32_t batch;                 /* B >= 1                                          */
   int32_t n_segments;            /* total segments over all requests                */
@@ -115,6 +125,7 @@ typedef struct c2kv_compose_desc {
   const int32_t* kept_idx;       /* strictly ascending within a segment, each in
                                     [0, seg_span); a segment may keep nothing       */
   int32_t key_encoding;          /* c2kv_key_encoding of the pool's keys            */
+  int32_t pool_layout;           /* c2kv_pool_layout                                */
 } c2kv_compose_desc;
 
 /* Launch-shape options.  Zero fields select the defaults. */
@@ -207,6 +218,24 @@ c2kv_status c2kv_attend(const c2kv_plan* plan, const void* k_pages, const void* 
 c2kv_status c2kv_compose_attend(const c2kv_plan* plan, const c2kv_pool* pool,
                                 const void* q, const void* k_suf, const void* v_suf,
                                 void* out, float* lse, void* stream);
+
+/* The load step (Appendix C: compressed caches move to the GPU before they are
+ * repositioned).  Page-locked host memory that kernels can also read in place:
+ * *host is its CPU address, *device the address to put in a c2kv_pool for
+ * reads over the host link (zero-copy).  Free with c2kv_host_free(host).
+ * C2KV_E_HIP if the runtime cannot provide it. */
+c2kv_status c2kv_host_alloc(size_t bytes, void** host, void** device);
+c2kv_status c2kv_host_free(void* host);
+
+/* Copy engines instead of zero-copy reads: for every segment of the plan the
+ * pool rows its kept tokens read (first to last; with a compressed pool exactly
+ * its kept rows; ranges of neighbouring segments merged) are copied from `src`
+ * to the same rows of `dst`, K and V (and the int8 scales), with asynchronous
+ * copies on `stream`.  src may be host (c2kv_host_alloc) or device memory; dst
+ * is a device pool of the same dtype with n_rows covering the plan.  Returns
+ * C2KV_E_INVAL on mismatched pools. */
+c2kv_status c2kv_load(const c2kv_plan* plan, const c2kv_pool* src, const c2kv_pool* dst,
+                      void* stream);
 
 /* Per-kernel timing for measurement: when enabled, every kernel is launched
  * with a pair of HIP events that its dispatch stamps at kernel start and end

@@ -107,7 +107,7 @@ def rope_rotate(x: np.ndarray, pos, base: float) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 def compose_layout(req_seg_off, seg_row0, seg_span, seg_orig_pos0, seg_kept_off,
-                   kept_idx, seg_new_pos0=None) -> dict:
+                   kept_idx, seg_new_pos0=None, compressed: bool = False) -> dict:
     """Walk each request's segments in order and list its composed slots.
 
     Segment c of a request starts at new_pos0_c = sum of the spans of the
@@ -118,6 +118,8 @@ def compose_layout(req_seg_off, seg_row0, seg_span, seg_orig_pos0, seg_kept_off,
         p_new   = new_pos0_c + j,  delta = new_pos0_c - orig_pos0_c.
     span_end of the request = start of the first position after its last span.
     Slot order = segments in request order, then kept indices ascending.
+    compressed=True reads a pool that stores each chunk compressed (only its
+    kept tokens, in order): the k-th kept token of a segment is row row0_c + k.
     """
     req_seg_off = np.asarray(req_seg_off, np.int64)
     B = len(req_seg_off) - 1
@@ -132,9 +134,9 @@ def compose_layout(req_seg_off, seg_row0, seg_span, seg_orig_pos0, seg_kept_off,
             span = int(seg_span[c])
             row0 = int(seg_row0[c])
             orig0 = int(seg_orig_pos0[c])
-            for j in kept_idx[int(seg_kept_off[c]):int(seg_kept_off[c + 1])]:
+            for k, j in enumerate(kept_idx[int(seg_kept_off[c]):int(seg_kept_off[c + 1])]):
                 j = int(j)
-                src.append(row0 + j)
+                src.append(row0 + (k if compressed else j))
                 seg.append(c)
                 po.append(orig0 + j)
                 pn.append(new0 + j)
@@ -235,7 +237,8 @@ def compose_attend(w, rows: Optional[Sequence[int]] = None, requests=None,
     """Whole path for a workload-like object `w` (attribute names of the C ABI's
     descriptor).  Returns (out [B][S'][H_q][d], lse [B][H_q][S'], layout)."""
     layout = compose_layout(w.req_seg_off, w.seg_row0, w.seg_span, w.seg_orig_pos0,
-                            w.seg_kept_off, w.kept_idx, w.seg_new_pos0)
+                            w.seg_kept_off, w.kept_idx, w.seg_new_pos0,
+                            compressed=getattr(w, "pool_compressed", False))
     B = len(layout["src_row"])
     reqs = range(B) if requests is None else requests
     sub = {k: [layout[k][r] for r in reqs] if isinstance(layout[k], list) else layout[k]

@@ -22,13 +22,15 @@ C2KV_OK, C2KV_E_INVAL, C2KV_E_UNSUPPORTED, C2KV_E_WORKSPACE, C2KV_E_HIP, C2KV_E_
     C2KV_E_STATE = 0, -1, -2, -3, -4, -5, -6
 C2KV_F32, C2KV_BF16, C2KV_I8 = 0, 1, 2
 C2KV_KEYS_ROPE_AT_ORIG, C2KV_KEYS_PRE_ROPE = 0, 1
+C2KV_POOL_FULL, C2KV_POOL_COMPRESSED = 0, 1
 _DTYPE_CODE = {"f32": C2KV_F32, "bf16": C2KV_BF16, "i8": C2KV_I8}
 
 EXPORTED = [
     "c2kv_plan_create", "c2kv_plan_destroy", "c2kv_plan_get_info", "c2kv_plan_get_requests",
     "c2kv_plan_get_slots", "c2kv_plan_get_block_table", "c2kv_plan_upload", "c2kv_compose",
     "c2kv_attend", "c2kv_compose_attend", "c2kv_timing_enable", "c2kv_timing_reset",
-    "c2kv_timing_read", "c2kv_last_error", "c2kv_version",
+    "c2kv_timing_read", "c2kv_last_error", "c2kv_version", "c2kv_host_alloc",
+    "c2kv_host_free", "c2kv_load",
 ]
 
 
@@ -49,7 +51,8 @@ class ComposeDesc(ctypes.Structure):
                 ("req_seg_off", ctypes.c_void_p), ("seg_row0", ctypes.c_void_p),
                 ("seg_span", ctypes.c_void_p), ("seg_orig_pos0", ctypes.c_void_p),
                 ("seg_new_pos0", ctypes.c_void_p), ("seg_kept_off", ctypes.c_void_p),
-                ("kept_idx", ctypes.c_void_p), ("key_encoding", ctypes.c_int32)]
+                ("kept_idx", ctypes.c_void_p), ("key_encoding", ctypes.c_int32),
+                ("pool_layout", ctypes.c_int32)]
 
 
 class PlanOpts(ctypes.Structure):
@@ -99,6 +102,9 @@ def _load() -> ctypes.CDLL:
         "c2kv_timing_read": [ctypes.c_char_p, P(ctypes.c_double), P(i64)],
         "c2kv_last_error": [],
         "c2kv_version": [],
+        "c2kv_host_alloc": [sz, P(vp), P(vp)],
+        "c2kv_host_free": [vp],
+        "c2kv_load": [vp, P(PoolDesc), P(PoolDesc), vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -152,7 +158,7 @@ class Plan:
                  seg_kept_off, kept_idx, suffix_len: int, seg_new_pos0=None,
                  softmax_scale: float = 0.0, page_size: int = 0, kv_splits: int = 0,
                  rows_per_block: int = 0, num_cus: int = 0, merge_mode: int = 0,
-                 keys_pre_rope: bool = False):
+                 keys_pre_rope: bool = False, pool_compressed: bool = False):
         self._arrays = dict(
             req_seg_off=np.ascontiguousarray(req_seg_off, np.int32),
             seg_row0=np.ascontiguousarray(seg_row0, np.int64),
@@ -171,7 +177,8 @@ class Plan:
                            _np_ptr(a["seg_span"]), _np_ptr(a["seg_orig_pos0"]),
                            _np_ptr(a["seg_new_pos0"]), _np_ptr(a["seg_kept_off"]),
                            _np_ptr(a["kept_idx"]), C2KV_KEYS_PRE_ROPE if keys_pre_rope
-                           else C2KV_KEYS_ROPE_AT_ORIG)
+                           else C2KV_KEYS_ROPE_AT_ORIG,
+                           C2KV_POOL_COMPRESSED if pool_compressed else C2KV_POOL_FULL)
         opts = PlanOpts(page_size, kv_splits, rows_per_block, num_cus, merge_mode)
         h = ctypes.c_void_p()
         _check(_lib.c2kv_plan_create(ctypes.byref(self.cfg), ctypes.byref(desc),
@@ -188,7 +195,8 @@ class Plan:
         return cls(w.n_q_heads, w.n_kv_heads, w.head_dim, w.act_dtype, w.rope_base,
                    w.req_seg_off, w.seg_row0, w.seg_span, w.seg_orig_pos0, w.seg_kept_off,
                    w.kept_idx, w.suffix_len, seg_new_pos0=w.seg_new_pos0,
-                   keys_pre_rope=getattr(w, "keys_pre_rope", False), **opts)
+                   keys_pre_rope=getattr(w, "keys_pre_rope", False),
+                   pool_compressed=getattr(w, "pool_compressed", False), **opts)
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -271,6 +279,45 @@ def c2kv_compose_attend(plan: Plan, pool: PoolDesc, q, k_suf, v_suf, out, lse=No
     _check(_lib.c2kv_compose_attend(plan.handle, ctypes.byref(pool), _dev_ptr(q),
                                     _dev_ptr(k_suf), _dev_ptr(v_suf), _dev_ptr(out),
                                     _dev_ptr(lse), _stream(stream)))
+
+
+def c2kv_load(plan: Plan, src: PoolDesc, dst: PoolDesc, stream=None):
+    _check(_lib.c2kv_load(plan.handle, ctypes.byref(src), ctypes.byref(dst), _stream(stream)))
+
+
+class HostPool:
+    """A pool in page-locked host memory from c2kv_host_alloc, filled from numpy
+    storage arrays (bf16 as uint16 bit patterns).  `desc` points kernels at it
+    for reads in place over the host link; it is also a c2kv_load source."""
+
+    def __init__(self, pool_k: np.ndarray, pool_v: np.ndarray, dtype: str,
+                 k_scale: Optional[np.ndarray] = None, v_scale: Optional[np.ndarray] = None):
+        self._host = []
+        code = {"f32": C2KV_F32, "bf16": C2KV_BF16, "i8": C2KV_I8}[dtype]
+        if pool_k.shape != pool_v.shape:
+            raise ValueError("pool K and V must have the same shape")
+        self.nbytes = 0
+        ptrs = [self._put(a) for a in (pool_k, pool_v, k_scale, v_scale)]
+        self.desc = PoolDesc(code, ptrs[0], ptrs[1], ptrs[2], ptrs[3], int(pool_k.shape[0]))
+
+    def _put(self, a: Optional[np.ndarray]):
+        if a is None:
+            return None
+        a = np.ascontiguousarray(a)
+        host, dev = ctypes.c_void_p(), ctypes.c_void_p()
+        _check(_lib.c2kv_host_alloc(max(a.nbytes, 1), ctypes.byref(host), ctypes.byref(dev)))
+        self._host.append(host)
+        ctypes.memmove(host, a.ctypes.data, a.nbytes)
+        self.nbytes += a.nbytes
+        return dev.value
+
+    def close(self):
+        lib_ = _lib
+        while self._host and lib_ is not None:
+            lib_.c2kv_host_free(self._host.pop())
+
+    def __del__(self):
+        self.close()
 
 
 def timing_enable(on: bool = True):

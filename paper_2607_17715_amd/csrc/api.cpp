@@ -290,6 +290,59 @@ c2kv_status c2kv_compose_attend(const c2kv_plan* plan, const c2kv_pool* pool, co
                        q, k_suf, v_suf, out, lse, stream);
 }
 
+c2kv_status c2kv_host_alloc(size_t bytes, void** host, void** device) {
+  if (!host || !device || bytes == 0) return fail(C2KV_E_INVAL, "host_alloc: bad arguments");
+  *host = nullptr;
+  *device = nullptr;
+  void* h = nullptr;
+  hipError_t e = hipHostMalloc(&h, bytes, hipHostMallocMapped);
+  if (e != hipSuccess) return hip_fail(e, "hipHostMalloc");
+  void* d = nullptr;
+  e = hipHostGetDevicePointer(&d, h, 0);
+  if (e != hipSuccess) {
+    (void)hipHostFree(h);
+    return hip_fail(e, "hipHostGetDevicePointer");
+  }
+  *host = h;
+  *device = d;
+  return C2KV_OK;
+}
+
+c2kv_status c2kv_host_free(void* host) {
+  if (!host) return C2KV_OK;
+  const hipError_t e = hipHostFree(host);
+  return e == hipSuccess ? C2KV_OK : hip_fail(e, "hipHostFree");
+}
+
+c2kv_status c2kv_load(const c2kv_plan* plan, const c2kv_pool* src, const c2kv_pool* dst,
+                      void* stream) {
+  c2kv_status st;
+  if (!check_plan(plan, &st)) return st;
+  const c2kv::Plan& p = plan->p;
+  if (!check_pool(p, src, &st) || !check_pool(p, dst, &st)) return st;
+  if (src->dtype != dst->dtype) return fail(C2KV_E_INVAL, "load: pools of different dtypes");
+  const size_t esz = src->dtype == C2KV_F32 ? 4 : src->dtype == C2KV_BF16 ? 2 : 1;
+  const size_t row_bytes = esz * size_t(p.cfg.n_kv_heads) * size_t(p.cfg.head_dim);
+  const size_t scale_bytes = sizeof(float) * size_t(p.cfg.n_kv_heads);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto copy = [&](const void* from, void* to, size_t per_row, int64_t r0, int64_t r1) {
+    return hipMemcpyAsync(static_cast<uint8_t*>(to) + size_t(r0) * per_row,
+                          static_cast<const uint8_t*>(from) + size_t(r0) * per_row,
+                          size_t(r1 - r0) * per_row, hipMemcpyDefault, s);
+  };
+  for (const auto& r : p.load_rows) {
+    hipError_t e = copy(src->k, const_cast<void*>(dst->k), row_bytes, r.first, r.second);
+    if (e == hipSuccess) e = copy(src->v, const_cast<void*>(dst->v), row_bytes, r.first, r.second);
+    if (e == hipSuccess && src->dtype == C2KV_I8) {
+      e = copy(src->k_scale, const_cast<float*>(dst->k_scale), scale_bytes, r.first, r.second);
+      if (e == hipSuccess)
+        e = copy(src->v_scale, const_cast<float*>(dst->v_scale), scale_bytes, r.first, r.second);
+    }
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (load)");
+  }
+  return C2KV_OK;
+}
+
 c2kv_status c2kv_timing_enable(int32_t on) {
   std::lock_guard<std::mutex> lk(g_timing.mu);
   g_timing.on = on != 0;

@@ -134,6 +134,11 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
     return C2KV_E_INVAL;
   }
   p.keys_pre_rope = d.key_encoding == C2KV_KEYS_PRE_ROPE;
+  if (d.pool_layout != C2KV_POOL_FULL && d.pool_layout != C2KV_POOL_COMPRESSED) {
+    err = "pool_layout must be C2KV_POOL_FULL or C2KV_POOL_COMPRESSED";
+    return C2KV_E_INVAL;
+  }
+  p.pool_compressed = d.pool_layout == C2KV_POOL_COMPRESSED;
   p.softmax_scale = cfg.softmax_scale > 0.f ? cfg.softmax_scale
                                             : static_cast<float>(1.0 / std::sqrt(double(cfg.head_dim)));
   p.qscale_log2 = static_cast<float>(double(p.softmax_scale) * 1.4426950408889634);
@@ -163,6 +168,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       }
       p.seg_delta[c] = static_cast<int32_t>(delta);
       int64_t prev = -1;
+      int64_t first_row = -1, last_row = -1;
       for (int k = d.seg_kept_off[c]; k < d.seg_kept_off[c + 1]; ++k) {
         const int64_t j = d.kept_idx[k];
         if (j < 0 || j >= span) {
@@ -174,7 +180,9 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
           return C2KV_E_INVAL;
         }
         prev = j;
-        const int64_t src = row0 + j;
+        const int64_t src = row0 + (p.pool_compressed ? int64_t(k - d.seg_kept_off[c]) : j);
+        if (first_row < 0) first_row = src;
+        last_row = src;
         if (src > kI32Max) { err = "pool row beyond int32 range"; return C2KV_E_UNSUPPORTED; }
         p.slot_src.push_back(static_cast<int32_t>(src));
         p.slot_seg.push_back(c);
@@ -182,6 +190,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
         p.slot_delta.push_back(static_cast<int32_t>(delta));
         p.max_src_row = std::max<int64_t>(p.max_src_row, src);
       }
+      if (first_row >= 0) p.load_rows.push_back({first_row, last_row + 1});
       cursor = new0 + span;               // span-preserving: advance by n, not m
       end = std::max(end, new0 + span);
     }
@@ -191,6 +200,19 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
     }
     p.span_end[b] = static_cast<int32_t>(end);
     p.req_slot0[b + 1] = static_cast<int32_t>(p.slot_src.size());
+  }
+
+  // rows the load step copies: segment ranges sorted and merged
+  std::sort(p.load_rows.begin(), p.load_rows.end());
+  {
+    std::vector<std::pair<int64_t, int64_t>> merged;
+    for (const auto& r : p.load_rows) {
+      if (!merged.empty() && r.first <= merged.back().second)
+        merged.back().second = std::max(merged.back().second, r.second);
+      else
+        merged.push_back(r);
+    }
+    p.load_rows.swap(merged);
   }
 
   // ---- pages: each request gets ceil(N_b / page) consecutive pages ----------

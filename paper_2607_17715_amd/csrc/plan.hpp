@@ -55,6 +55,8 @@ struct Plan {
   int32_t batch = 0, suffix_len = 0, page_size = 64, n_segments = 0;
   int32_t group = 1;               // G = H_q / H_kv
   bool keys_pre_rope = false;      // pool keys stored before RoPE: per-slot cos/sin rows
+  bool pool_compressed = false;    // slot k of a segment reads row seg_row0 + k
+  std::vector<std::pair<int64_t, int64_t>> load_rows;   // merged [first, end) row ranges
   float qscale_log2 = 0.f;         // softmax scale * log2(e)
   float softmax_scale = 0.f;
 

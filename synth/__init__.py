@@ -117,6 +117,7 @@ class Workload:
     k_suf: np.ndarray
     v_suf: np.ndarray
     keys_pre_rope: bool = False  # pool keys taken as stored before RoPE (same values)
+    pool_compressed: bool = False  # pool holds only kept rows, chunk by chunk
 
     @property
     def batch(self) -> int:
@@ -301,6 +302,30 @@ def small(pool_dtype="bf16", act_dtype=None, n_q_heads=8, n_kv_heads=2, head_dim
               n_pool_chunks, chunk_len, prefix_len, batch, chunks_per_req, order, keep,
               suffix_len)
     return build(sp, layer=layer, seed=seed)
+
+
+def compress_pool(w: Workload) -> Workload:
+    """The same workload with its pool stored compressed: each distinct chunk
+    (segment row0) keeps only its kept rows, in order, and segments point at
+    their chunk's first kept row.  Values are copied, not redrawn, so results
+    equal those of the full pool."""
+    first_of = {}
+    rows = []
+    new_row0 = np.zeros_like(w.seg_row0)
+    for c in range(w.n_segments):
+        row0 = int(w.seg_row0[c])
+        kept = w.kept_idx[w.seg_kept_off[c]:w.seg_kept_off[c + 1]].astype(np.int64)
+        key = (row0, tuple(kept.tolist()))
+        if key not in first_of:
+            first_of[key] = sum(len(r) for r in rows)
+            rows.append(row0 + kept)
+        new_row0[c] = first_of[key]
+    idx = np.concatenate(rows) if rows else np.zeros(0, np.int64)
+    take = lambda a: None if a is None else np.ascontiguousarray(a[idx])
+    return dataclasses.replace(w, pool_k=take(w.pool_k), pool_v=take(w.pool_v),
+                               pool_k_scale=take(w.pool_k_scale),
+                               pool_v_scale=take(w.pool_v_scale), seg_row0=new_row0,
+                               pool_compressed=True)
 
 
 def with_overrides(w: Workload, **kw) -> Workload:

@@ -268,6 +268,24 @@ def test_pre_rope_keys_encoded_at_new_positions(seed, keep):
     assert np.abs(other - out).max() > 1e-3
 
 
+@pytest.mark.parametrize("keep", [("ratio", 0.1, 0.6), ("c2", 4), ("none",)])
+def test_compressed_pool_reads_the_same_tokens(keep):
+    """A chunk stored compressed (Section 3.2: only its kept tokens are saved)
+    holds the k-th kept token in row k: the composed result equals that of the
+    whole chunk with kept index j in row j, for every request of a batch that
+    reuses chunks."""
+    w = synth.small(pool_dtype="f32", keep=keep, batch=3, n_pool_chunks=4, chunks_per_req=3,
+                    head_dim=16, n_q_heads=4, n_kv_heads=2, suffix_len=5, chunk_len=40)
+    wc = synth.compress_pool(w)
+    assert wc.pool_k.shape[0] == sum(
+        len(set(map(int, w.kept_idx[w.seg_kept_off[c]:w.seg_kept_off[c + 1]])))
+        for c in sorted({int(r): i for i, r in enumerate(w.seg_row0)}.values()))
+    a, la, _ = oracle.compose_attend(w)
+    b, lb, _ = oracle.compose_attend(wc)
+    np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(la, lb)
+
+
 def test_fixed_pos_ablation_differs():
     """Section 4.8 (Fixed-Pos): without re-rotation the result changes."""
     w = synth.small(pool_dtype="f32", head_dim=16, suffix_len=4, batch=1)

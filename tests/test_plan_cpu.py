@@ -32,7 +32,9 @@ def _oracle_layout(w):
 
 
 def _assert_layout_equal(w, plan):
-    lay = _oracle_layout(w)
+    lay = oracle.compose_layout(w.req_seg_off, w.seg_row0, w.seg_span, w.seg_orig_pos0,
+                                w.seg_kept_off, w.kept_idx, w.seg_new_pos0,
+                                compressed=w.pool_compressed)
     n, e = plan.requests()
     assert list(n) == list(map(int, lay["composed_len"]))
     assert list(e) == list(map(int, lay["span_end"]))
@@ -46,6 +48,14 @@ def _assert_layout_equal(w, plan):
 def test_layout_bit_exact_configs(idx):
     w = synth.config(idx)
     _assert_layout_equal(w, c2kv.Plan.for_workload(w))
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4])
+def test_layout_bit_exact_compressed_pools(idx):
+    w = synth.compress_pool(synth.config(idx))
+    plan = c2kv.Plan.for_workload(w)
+    _assert_layout_equal(w, plan)
+    assert plan.info["max_src_row"] == w.pool_k.shape[0] - 1
 
 
 def test_layout_bit_exact_ragged_and_edges():
@@ -150,18 +160,20 @@ def test_validation_errors():
     _expect_status(E.C2KV_E_UNSUPPORTED, mk(seg_row0=row0))
 
 
-def test_key_encoding_is_validated():
+def test_key_encoding_and_pool_layout_are_validated():
     w = synth.small(batch=1)
     a = {k: np.ascontiguousarray(getattr(w, k)) for k in
          ("req_seg_off", "seg_row0", "seg_span", "seg_orig_pos0", "seg_kept_off", "kept_idx")}
     cfg = c2kv.AttnCfg(w.n_q_heads, w.n_kv_heads, w.head_dim, c2kv.C2KV_BF16, w.rope_base, 0.0)
     ptr = lambda x: x.ctypes.data_as(ctypes.c_void_p)
-    for enc, want in ((c2kv.C2KV_KEYS_ROPE_AT_ORIG, c2kv.C2KV_OK),
-                      (c2kv.C2KV_KEYS_PRE_ROPE, c2kv.C2KV_OK), (2, c2kv.C2KV_E_INVAL),
-                      (-1, c2kv.C2KV_E_INVAL)):
+    for enc, lay, want in ((c2kv.C2KV_KEYS_ROPE_AT_ORIG, 0, c2kv.C2KV_OK),
+                           (c2kv.C2KV_KEYS_PRE_ROPE, 0, c2kv.C2KV_OK),
+                           (0, c2kv.C2KV_POOL_COMPRESSED, c2kv.C2KV_OK),
+                           (2, 0, c2kv.C2KV_E_INVAL), (-1, 0, c2kv.C2KV_E_INVAL),
+                           (0, 2, c2kv.C2KV_E_INVAL), (0, -1, c2kv.C2KV_E_INVAL)):
         desc = c2kv.ComposeDesc(w.batch, w.n_segments, ptr(a["req_seg_off"]), ptr(a["seg_row0"]),
                                 ptr(a["seg_span"]), ptr(a["seg_orig_pos0"]), None,
-                                ptr(a["seg_kept_off"]), ptr(a["kept_idx"]), enc)
+                                ptr(a["seg_kept_off"]), ptr(a["kept_idx"]), enc, lay)
         h = ctypes.c_void_p()
         st = c2kv.lib().c2kv_plan_create(ctypes.byref(cfg), ctypes.byref(desc), w.suffix_len,
                                          None, ctypes.byref(h))
