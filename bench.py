@@ -54,7 +54,10 @@ WORKLOADS = {
     "llama3-8b-layer-host-load": 2,
     "int8-layer-host-zerocopy": 4,
     "int8-layer-host-load": 4,
+    "sif-extract-llama3-8b-bf16": 0,
 }
+# extraction-time attention with Structured Information Flow over document chunks
+SIF = {"sif-extract-llama3-8b-bf16"}
 DEFAULT_WORKLOAD = "llama3-8b-layer-bf16"
 LONG_SUFFIX = {"70b-long-suffix-bf16"}
 # one generated token over a cache composed once beforehand: the step is c2kv_attend
@@ -162,6 +165,146 @@ def cpu_baseline(w, idx: int):
             "kind": "oracle", "sample": sample, "seconds_per_layer": per_layer}
 
 
+def time_steps(step, copies, args, c2kv, torch):
+    """Warm-up, an eager timing, the timed graph replays (K steps captured over the
+    input copies), and a pass with per-kernel dispatch-stamped events.  Returns
+    (ms per step, eager ms per step, per-kernel averages, whether graphs ran)."""
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    K = args.steps
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ke = min(K, 256)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(ke):
+        step(i)
+    end.record()
+    torch.cuda.synchronize()
+    eager_ms = start.elapsed_time(end) / ke
+    graph_used = not args.no_graph
+    if graph_used:
+        n_full, rem = divmod(K, copies)
+        g_full = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_full):
+            for i in range(copies):
+                step(i)
+        g_rem = None
+        if rem:
+            g_rem = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_rem):
+                for i in range(rem):
+                    step(i)
+        g_full.replay()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(n_full):
+            g_full.replay()
+        if g_rem is not None:
+            g_rem.replay()
+        end.record()
+        torch.cuda.synchronize()
+        total_ms = start.elapsed_time(end)
+    else:
+        torch.cuda.synchronize()
+        start.record()
+        for i in range(K):
+            step(i)
+        end.record()
+        torch.cuda.synchronize()
+        total_ms = start.elapsed_time(end)
+    c2kv.timing_reset()
+    c2kv.timing_enable(True)
+    for i in range(ke):
+        step(i)
+    torch.cuda.synchronize()
+    c2kv.timing_enable(False)
+    kern = {}
+    for name in ("compose", "attn_paged", "attn_pool", "merge"):
+        ms, n = c2kv.timing_read(name)
+        if n:
+            kern[name] = {"avg_us": 1e3 * ms / n, "launches": n}
+    c2kv.timing_reset()
+    return total_ms / K, eager_ms, kern, graph_used
+
+
+def run_sif(args, c2kv, synth, torch):
+    """Extraction-time SIF attention: the value counts the tokens of the extraction
+    sequences (originals and C^2 tokens) per second and layer."""
+    import oracle
+    w = synth.sif_config(args.workload)
+    plan = c2kv.Plan.for_sif(w, kv_splits=args.kv_splits, rows_per_block=args.rows_per_block,
+                             merge_mode=args.merge_mode).upload()
+    B, L, Hq, Hkv, D = w.batch, w.seq_len, w.n_q_heads, w.n_kv_heads, w.head_dim
+    b_act = 4 if w.act_dtype == "f32" else 2
+    vis = oracle.sif_mask(w.n_tokens, w.block, w.sink)
+    pairs = int(vis.sum()) * B
+    byts = B * L * ((2 * Hq + 2 * Hkv) * D * b_act + 4 * Hq)     # q, k, v, out, lse
+    flops = 4 * Hq * D * pairs
+    base = dict(q=c2kv.to_device(w.q, w.act_dtype), k=c2kv.to_device(w.k, w.act_dtype),
+                v=c2kv.to_device(w.v, w.act_dtype))
+    footprint = sum(t.numel() * t.element_size() for t in base.values())
+    copies = args.copies or int(min(64, max(2, math.ceil(2.2 * MALL_BYTES / footprint))))
+    sets = [base] + [{k: t.clone() for k, t in base.items()} for _ in range(copies - 1)]
+    for s in sets:
+        s["out"] = torch.empty_like(s["q"])
+        s["lse"] = torch.empty((B, Hq, L), dtype=torch.float32, device="cuda")
+
+    def step(i):
+        s = sets[i % copies]
+        c2kv.c2kv_attend(plan, None, None, s["q"], s["k"], s["v"], s["out"], s["lse"])
+
+    ms_per_step, eager_ms, kern, graph_used = time_steps(step, copies, args, c2kv, torch)
+    assert torch.isfinite(sets[0]["out"]).all().item(), "non-finite output"
+    dom_s = kern["attn_paged"]["avg_us"] * 1e-6
+    t_hbm, t_mfma = byts / (PEAK_HBM_GBS * 1e9), flops / (PEAK_BF16_TFLOPS * 1e12)
+    if t_hbm >= t_mfma:
+        roof = {"bound": "hbm", "achieved": byts / dom_s / 1e9, "peak": PEAK_HBM_GBS,
+                "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": flops / dom_s / 1e12, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof.update(traffic=load_traffic(args.workload, "attn_paged", byts), kernel="attn_paged",
+                kernel_avg_us=kern["attn_paged"]["avg_us"], algorithmic_bytes=byts,
+                algorithmic_flops=flops)
+    result = {
+        "metric": METRIC, "value": B * L / (ms_per_step * 1e-3), "unit": "tokens/s/layer",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if w.act_dtype == "f32" else "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "n_q_heads": Hq, "n_kv_heads": Hkv,
+                   "head_dim": D, "batch": B, "n_tokens": w.n_tokens, "block": w.block,
+                   "sink": w.sink, "sequence_tokens": B * L,
+                   "path": "SIF extraction attention (c2kv_attend with a SIF plan)",
+                   "plan": {k: plan.info[k] for k in ("rows_per_block", "n_work_items",
+                                                      "n_merge_groups", "max_splits")},
+                   "input_copies": copies, "graph": graph_used},
+        "roofline": roof, "kernels_us": kern, "eager_ms_per_step": eager_ms,
+        "source_sha": kernel_source_sha(),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the float64 oracle on the host (cpu_baseline)")
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            q, k, v = (oracle.decode_storage(x[reps % B], w.act_dtype) for x in (w.q, w.k, w.v))
+            oracle.sif_attend(q, k, v, w.n_tokens, w.block, w.sink, w.rope_base)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el > 10.0 or reps >= 4 * B:
+                break
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            threads = 1
+        result["cpu_baseline"] = {"value": reps * L / el, "unit": "tokens/s/layer",
+                                  "cores": int(threads), "kind": "oracle",
+                                  "sample": f"{reps} whole sequences of {L} tokens"}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -181,8 +324,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the compose-and-attend path here runs on a single "
-              "MI355X (--gpus 1); multi-GPU sharding is described in DESIGN.md, not built.",
-              file=sys.stderr)
+              "MI355X (--gpus 1); sharding over several GPUs is not built.", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -199,6 +341,8 @@ def main():
         log(f"calibration copy of {n} bytes done")
         del src, dst
 
+    if args.workload in SIF:
+        return run_sif(args, c2kv, synth, torch)
     idx = WORKLOADS[args.workload]
     log(f"workload {args.workload}: generating inputs")
     w = synth.config(idx)
@@ -282,73 +426,11 @@ def main():
             c2kv.c2kv_compose_attend(plan, s["pool"], s["q"], s["k_suf"], s["v_suf"], s["out"],
                                      s["lse"])
 
-    # ---- warmup (eager)
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
+    ms_per_step, eager_ms, kern, graph_used = time_steps(step, copies, args, c2kv, torch)
     assert torch.isfinite(sets[0]["out"]).all().item(), "non-finite output"
-
     K = args.steps
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
-    # ---- eager timing (reported beside the graph number)
-    ke = min(K, 256)
-    torch.cuda.synchronize()
-    start.record()
-    for i in range(ke):
-        step(i)
-    end.record()
-    torch.cuda.synchronize()
-    eager_ms = start.elapsed_time(end) / ke
-
-    # ---- timed region: K steps replayed from graphs captured over the copies
-    graph_used = not args.no_graph
-    if graph_used:
-        n_full, rem = divmod(K, copies)
-        g_full = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g_full):
-            for i in range(copies):
-                step(i)
-        g_rem = None
-        if rem:
-            g_rem = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g_rem):
-                for i in range(rem):
-                    step(i)
-        g_full.replay()
-        torch.cuda.synchronize()
-        start.record()
-        for _ in range(n_full):
-            g_full.replay()
-        if g_rem is not None:
-            g_rem.replay()
-        end.record()
-        torch.cuda.synchronize()
-        total_ms = start.elapsed_time(end)
-    else:
-        torch.cuda.synchronize()
-        start.record()
-        for i in range(K):
-            step(i)
-        end.record()
-        torch.cuda.synchronize()
-        total_ms = start.elapsed_time(end)
-    ms_per_step = total_ms / K
     value = work["tokens"] / (ms_per_step * 1e-3)
-
-    # ---- per-kernel durations (HIP events around each launch, on its stream)
-    c2kv.timing_reset()
-    c2kv.timing_enable(True)
-    for i in range(ke):
-        step(i)
-    torch.cuda.synchronize()
-    c2kv.timing_enable(False)
-    kern = {}
-    for name in ("compose", "attn_paged", "attn_pool", "merge"):
-        ms, n = c2kv.timing_read(name)
-        if n:
-            kern[name] = {"avg_us": 1e3 * ms / n, "launches": n}
-    c2kv.timing_reset()
 
     dom = "attn_paged" if paged else "attn_pool"
     dom_s = kern[dom]["avg_us"] * 1e-6

@@ -219,6 +219,22 @@ c2kv_status c2kv_compose_attend(const c2kv_plan* plan, const c2kv_pool* pool,
                                 const void* q, const void* k_suf, const void* v_suf,
                                 void* out, float* lse, void* stream);
 
+/* Extraction-time attention with Structured Information Flow (Section 3.3):
+ * each of `batch` sequences holds n_tokens original tokens followed by one C^2
+ * token per block of `block` originals, m = ceil(n_tokens / block) of them.  The
+ * plan is used with c2kv_plan_upload and c2kv_attend (k_pages = v_pages = NULL):
+ * q [batch][n+m][H_q][D], k_suf and v_suf [batch][n+m][H_kv][D] (all tokens,
+ * before RoPE), out [batch][n+m][H_q][D], lse [batch][H_q][n+m].  RoPE puts
+ * original token t at position t and C^2 token j at the position of the last
+ * token of its block, min((j+1) block, n) - 1.  The mask (Section 3.3.2):
+ * originals attend causally to originals only; C^2 token j attends to the
+ * originals of its block, to the first `sink` originals (the sink block B(0),
+ * whose size the paper leaves open), and to C^2 tokens 0..j.  C2KV_E_INVAL for
+ * batch, n_tokens or block < 1, or sink outside [0, n_tokens]. */
+c2kv_status c2kv_sif_plan_create(const c2kv_attn_cfg* cfg, int32_t batch, int32_t n_tokens,
+                                 int32_t block, int32_t sink, const c2kv_plan_opts* opts,
+                                 c2kv_plan** out);
+
 /* The load step (Appendix C: compressed caches move to the GPU before they are
  * repositioned).  Page-locked host memory that kernels can also read in place:
  * *host is its CPU address, *device the address to put in a c2kv_pool for

@@ -6,5 +6,5 @@ the HIP library or its Python binding.
 """
 from .c2kv_oracle import (  # noqa: F401
     decode_bf16, decode_storage, rope_theta, rope_rotate, compose_layout,
-    compose, attend, compose_attend, merge_partials,
+    compose, attend, compose_attend, merge_partials, sif_positions, sif_mask, sif_attend,
 )

@@ -260,6 +260,67 @@ def compose_attend(w, rows: Optional[Sequence[int]] = None, requests=None,
 
 
 # ---------------------------------------------------------------------------
+# extraction-time attention with Structured Information Flow (Section 3.3)
+# ---------------------------------------------------------------------------
+
+def sif_positions(n: int, block: int) -> np.ndarray:
+    """Positions of the sequence [x_1..x_n | c_1..c_m], m = ceil(n / block),
+    0-based: original token t at t; C^2 token c_j (one per block of `block`
+    originals) at the position of the last token of its block (Section 3.3.1)."""
+    m = -(-n // block)
+    j = np.arange(m)
+    return np.concatenate([np.arange(n), np.minimum((j + 1) * block, n) - 1]).astype(np.int64)
+
+
+def sif_mask(n: int, block: int, sink: int) -> np.ndarray:
+    """visible[t, u] over the same sequence (Section 3.3.2): an original token
+    sees the originals up to itself and no C^2 token; C^2 token c_j sees the
+    originals of its block B(j) and of the sink block B(0) (here the first `sink`
+    originals) and the C^2 tokens c_1..c_j."""
+    m = -(-n // block)
+    L = n + m
+    vis = np.zeros((L, L), bool)
+    for t in range(n):
+        vis[t, :t + 1] = True
+    for j in range(m):
+        row = n + j
+        vis[row, j * block:min((j + 1) * block, n)] = True
+        vis[row, :sink] = True
+        vis[row, n:n + j + 1] = True
+    return vis
+
+
+def sif_attend(q, k, v, n: int, block: int, sink: int, base: float,
+               scale: Optional[float] = None):
+    """One sequence of n originals and their C^2 tokens.  q [L, H_q, d],
+    k, v [L, H_kv, d] before RoPE, L = n + ceil(n / block).  Returns
+    out [L, H_q, d] and lse [H_q, L]."""
+    q = np.asarray(q, np.float64)
+    L, Hq, d = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    scale = 1.0 / math.sqrt(d) if scale is None or scale <= 0 else float(scale)
+    pos = sif_positions(n, block)
+    assert len(pos) == L
+    q_rot = rope_rotate(q, pos[:, None] * np.ones((1, Hq)), base)
+    k_rot = rope_rotate(np.asarray(k, np.float64), pos[:, None] * np.ones((1, Hkv)), base)
+    vals = np.asarray(v, np.float64)
+    vis = sif_mask(n, block, sink)
+    out = np.zeros((L, Hq, d))
+    lse = np.zeros((Hq, L))
+    for h in range(Hq):
+        g = h // G
+        s = scale * (q_rot[:, h, :] @ k_rot[:, g, :].T)
+        s = np.where(vis, s, -np.inf)
+        mx = s.max(axis=1, keepdims=True)
+        e = np.exp(s - mx)
+        z = e.sum(axis=1, keepdims=True)
+        out[:, h, :] = (e / z) @ vals[:, g, :]
+        lse[h, :] = (mx + np.log(z))[:, 0]
+    return out, lse
+
+
+# ---------------------------------------------------------------------------
 # combining attention over a partition of the keys
 # ---------------------------------------------------------------------------
 

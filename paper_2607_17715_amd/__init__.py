@@ -30,7 +30,7 @@ EXPORTED = [
     "c2kv_plan_get_slots", "c2kv_plan_get_block_table", "c2kv_plan_upload", "c2kv_compose",
     "c2kv_attend", "c2kv_compose_attend", "c2kv_timing_enable", "c2kv_timing_reset",
     "c2kv_timing_read", "c2kv_last_error", "c2kv_version", "c2kv_host_alloc",
-    "c2kv_host_free", "c2kv_load",
+    "c2kv_host_free", "c2kv_load", "c2kv_sif_plan_create",
 ]
 
 
@@ -105,6 +105,7 @@ def _load() -> ctypes.CDLL:
         "c2kv_host_alloc": [sz, P(vp), P(vp)],
         "c2kv_host_free": [vp],
         "c2kv_load": [vp, P(PoolDesc), P(PoolDesc), vp],
+        "c2kv_sif_plan_create": [P(AttnCfg), i32, i32, i32, i32, P(PlanOpts), P(vp)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -189,6 +190,36 @@ class Plan:
         inf = PlanInfo()
         _check(_lib.c2kv_plan_get_info(self._h, ctypes.byref(inf)))
         self.info = inf.as_dict()
+
+    @classmethod
+    def sif(cls, n_q_heads: int, n_kv_heads: int, head_dim: int, act_dtype: str,
+            rope_base: float, batch: int, n_tokens: int, block: int, sink: int,
+            softmax_scale: float = 0.0, page_size: int = 0, kv_splits: int = 0,
+            rows_per_block: int = 0, num_cus: int = 0, merge_mode: int = 0) -> "Plan":
+        """Plan of extraction-time SIF attention (c2kv_sif_plan_create); run it with
+        c2kv_attend(plan, None, None, q, k, v, out, lse)."""
+        self = cls.__new__(cls)
+        self._arrays = {}
+        self.cfg = AttnCfg(n_q_heads, n_kv_heads, head_dim, _DTYPE_CODE[act_dtype],
+                           float(rope_base), float(softmax_scale))
+        self.act_dtype = act_dtype
+        opts = PlanOpts(page_size, kv_splits, rows_per_block, num_cus, merge_mode)
+        h = ctypes.c_void_p()
+        _check(_lib.c2kv_sif_plan_create(ctypes.byref(self.cfg), int(batch), int(n_tokens),
+                                         int(block), int(sink), ctypes.byref(opts),
+                                         ctypes.byref(h)))
+        self._h = h
+        self.workspace = None
+        inf = PlanInfo()
+        _check(_lib.c2kv_plan_get_info(self._h, ctypes.byref(inf)))
+        self.info = inf.as_dict()
+        self.suffix_len = self.info["suffix_len"]
+        return self
+
+    @classmethod
+    def for_sif(cls, w, **opts) -> "Plan":
+        return cls.sif(w.n_q_heads, w.n_kv_heads, w.head_dim, w.act_dtype, w.rope_base,
+                       w.batch, w.n_tokens, w.block, w.sink, **opts)
 
     @classmethod
     def for_workload(cls, w, **opts) -> "Plan":

@@ -151,6 +151,28 @@ c2kv_status c2kv_plan_create(const c2kv_attn_cfg* cfg, const c2kv_compose_desc* 
   return C2KV_OK;
 }
 
+c2kv_status c2kv_sif_plan_create(const c2kv_attn_cfg* cfg, int32_t batch, int32_t n_tokens,
+                                 int32_t block, int32_t sink, const c2kv_plan_opts* opts,
+                                 c2kv_plan** out) {
+  if (!cfg || !out) return fail(C2KV_E_INVAL, "cfg and out must not be NULL");
+  c2kv_plan* plan = new (std::nothrow) c2kv_plan;
+  if (!plan) return fail(C2KV_E_NOMEM, "cannot allocate plan");
+  std::string err;
+  c2kv_status st;
+  try {
+    st = c2kv::build_sif_plan(*cfg, batch, n_tokens, block, sink, opts, plan->p, err);
+  } catch (const std::bad_alloc&) {
+    st = C2KV_E_NOMEM;
+    err = "host allocation failed while building the plan";
+  }
+  if (st != C2KV_OK) {
+    delete plan;
+    return fail(st, err);
+  }
+  *out = plan;
+  return C2KV_OK;
+}
+
 void c2kv_plan_destroy(c2kv_plan* plan) { delete plan; }
 
 c2kv_status c2kv_plan_get_info(const c2kv_plan* plan, c2kv_plan_info* info) {

@@ -221,6 +221,7 @@ __device__ inline uint4 keep_first(uint4 v, int n_keep) {
 
 struct AttnParams {
   int Hq, Hkv, G, S, PS, max_pages, RB, n_seg, merge_in_kernel;
+  int sif_n, sif_block, sif_sink;  // SIF mask over the suffix when sif_n > 0
   float qscale;                 // softmax scale * log2(e)
   const int* req_slot0;
   const int2* slot_info;        // (pool row, segment) per composed slot
@@ -299,6 +300,16 @@ struct Shape {
   static constexpr int RKW = imax(NKU * 2 * WA, PAGED ? NPK * 4 : NKU * 2 * WP);
   static constexpr int RVW = imax(NVU * 2 * WA, PAGED ? NPV * 4 : NVU * 2 * WP);
 };
+
+// Structured Information Flow mask over the sequence [n originals | C^2 tokens]:
+// an original sees earlier originals; C^2 token j sees the originals of its
+// block, the sink (the first sif_sink originals) and C^2 tokens 0..j.
+__device__ inline bool sif_visible(int t, int u, const AttnParams& a) {
+  if (t < a.sif_n) return u <= t;
+  const int j = t - a.sif_n;
+  if (u >= a.sif_n) return u - a.sif_n <= j;
+  return u < a.sif_sink || u / a.sif_block == j;
+}
 
 // ----------------------------------------------------------------------------
 // log-sum-exp combine of the key splits of one row block (rows [rlo, rhi))
@@ -799,7 +810,9 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int key = (kh * NKB + j) * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-          const bool vis = key < nvalid && (!suffix || k0 + key <= t);
+          const int u = k0 + key;
+          const bool vis = key < nvalid && (!suffix || (a.sif_n > 0 ? sif_visible(t, u, a)
+                                                                      : u <= t));
           if (!vis) s[j][v] = kNegInf;
         }
     }
@@ -1288,6 +1301,9 @@ hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const vo
   ap.RB = p.rows_per_block;
   ap.n_seg = p.n_segments;
   ap.merge_in_kernel = p.merge_in_kernel ? 1 : 0;
+  ap.sif_n = p.sif_n;
+  ap.sif_block = p.sif_block;
+  ap.sif_sink = p.sif_sink;
   ap.qscale = p.qscale_log2;
   ap.req_slot0 = at<int>(ws, p.ws.req_slot0);
   ap.slot_info = at<int2>(ws, p.ws.slot_info);

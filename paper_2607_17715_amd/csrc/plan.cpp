@@ -38,7 +38,7 @@ std::vector<double> rope_theta(int D, double base) {
 
 c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
                        int32_t suffix_len, const c2kv_plan_opts* opts, Plan& p,
-                       std::string& err) {
+                       std::string& err, const SifShape* sif) {
   // ---- attention shape ----------------------------------------------------
   if (cfg.n_q_heads < 1 || cfg.n_kv_heads < 1 || cfg.n_q_heads % cfg.n_kv_heads != 0) {
     err = fmt("n_q_heads (", cfg.n_q_heads, ") must be a positive multiple of n_kv_heads (",
@@ -250,7 +250,12 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   const int wgs_per_cu = 1;           // 8 wavefronts at 2 per SIMD fill a CU
   const int64_t target = int64_t(o.num_cus) * wgs_per_cu;
   const int32_t n_rb = ceil_div(R, RB);
-  struct Group { int32_t b, g, row0, nrows, tiles; };
+  // A group is one row block of one (request, kv-head) and the key tiles it reads
+  // (composed tiles first, then suffix tiles), as a list of [first, end) ranges.
+  struct Group {
+    int32_t b, g, row0, nrows, tiles;
+    std::vector<std::pair<int32_t, int32_t>> ranges;
+  };
   std::vector<Group> groups;
   int64_t total_tiles = 0;
   for (int b = 0; b < B; ++b) {
@@ -260,10 +265,31 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       for (int rb = 0; rb < n_rb; ++rb) {
         const int32_t row0 = rb * RB;
         const int32_t nrows = static_cast<int32_t>(std::min<int64_t>(RB, R - row0));
-        const int64_t tmax = (row0 + nrows - 1) / G;       // last suffix token in block
-        const int32_t nst = ceil_div(tmax + 1, kKeyTile);
-        groups.push_back({b, g, row0, nrows, nct + nst});
-        total_tiles += nct + nst;
+        const int64_t tmin = row0 / G, tmax = (row0 + nrows - 1) / G;   // suffix tokens
+        Group gr{b, g, row0, nrows, 0, {}};
+        if (sif && tmin >= sif->n_tokens) {
+          // C^2 rows only: the sink, the blocks of these C^2 tokens, and the C^2
+          // tokens up to the last of them (keys are suffix tiles: nct = 0)
+          const int64_t j0 = tmin - sif->n_tokens, j1 = tmax - sif->n_tokens;
+          std::vector<std::pair<int32_t, int32_t>> r;
+          if (sif->sink > 0) r.push_back({0, ceil_div(sif->sink, kKeyTile)});
+          r.push_back({static_cast<int32_t>(j0 * sif->block / kKeyTile),
+                       ceil_div(std::min<int64_t>((j1 + 1) * sif->block, sif->n_tokens), kKeyTile)});
+          r.push_back({static_cast<int32_t>(sif->n_tokens / kKeyTile),
+                       ceil_div(sif->n_tokens + j1 + 1, kKeyTile)});
+          std::sort(r.begin(), r.end());
+          for (const auto& x : r) {
+            if (!gr.ranges.empty() && x.first <= gr.ranges.back().second)
+              gr.ranges.back().second = std::max(gr.ranges.back().second, x.second);
+            else
+              gr.ranges.push_back(x);
+          }
+        } else {
+          gr.ranges.push_back({0, nct + ceil_div(tmax + 1, kKeyTile)});
+        }
+        for (const auto& x : gr.ranges) gr.tiles += x.second - x.first;
+        total_tiles += gr.tiles;
+        groups.push_back(std::move(gr));
       }
   }
   // Key splits only add parallelism where the row blocks alone leave CUs idle;
@@ -274,8 +300,16 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       split ? std::max<int64_t>(2, (total_tiles + target - 1) / target) : INT32_MAX;
   std::vector<WorkItem> items;
   for (const Group& gr : groups) {
-    int32_t ns = o.kv_splits > 0 ? o.kv_splits : ceil_div(gr.tiles, per_item);
-    ns = std::max(1, std::min({ns, gr.tiles, kMaxSplits}));
+    // splits of each range, at most kMaxSplits in all
+    std::vector<int32_t> nsr;
+    int32_t ns = 0;
+    for (const auto& x : gr.ranges) {
+      const int32_t len = x.second - x.first;
+      int32_t k = o.kv_splits > 0 ? o.kv_splits : ceil_div(len, per_item);
+      k = std::max(1, std::min({k, len, kMaxSplits / int32_t(gr.ranges.size())}));
+      nsr.push_back(k);
+      ns += k;
+    }
     p.max_splits = std::max(p.max_splits, ns);
     int32_t part0 = -1, merge = -1;
     if (ns > 1) {
@@ -284,11 +318,15 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       p.merges.push_back({gr.b, gr.g, gr.row0, gr.nrows, part0, ns, 0, 0});
       p.n_partials += ns;
     }
-    for (int s = 0; s < ns; ++s) {
-      const int32_t t0 = static_cast<int32_t>(int64_t(gr.tiles) * s / ns);
-      const int32_t t1 = static_cast<int32_t>(int64_t(gr.tiles) * (s + 1) / ns);
-      items.push_back({gr.b, gr.g, gr.row0, gr.nrows, t0, t1, ns > 1 ? part0 + s : -1, merge,
-                       p.req_slot0[gr.b], p.req_slot0[gr.b + 1] - p.req_slot0[gr.b], 0, 0});
+    int32_t k = 0;
+    for (size_t ri = 0; ri < gr.ranges.size(); ++ri) {
+      const int32_t first = gr.ranges[ri].first, len = gr.ranges[ri].second - first;
+      for (int s = 0; s < nsr[ri]; ++s, ++k) {
+        const int32_t t0 = first + static_cast<int32_t>(int64_t(len) * s / nsr[ri]);
+        const int32_t t1 = first + static_cast<int32_t>(int64_t(len) * (s + 1) / nsr[ri]);
+        items.push_back({gr.b, gr.g, gr.row0, gr.nrows, t0, t1, ns > 1 ? part0 + k : -1, merge,
+                         p.req_slot0[gr.b], p.req_slot0[gr.b + 1] - p.req_slot0[gr.b], 0, 0});
+      }
     }
   }
   // the in-kernel merge serialises a row block's combine in one workgroup,
@@ -386,16 +424,50 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       seg_cs[(size_t(c) * H + i) * 2 + 1] = static_cast<float>(std::sin(ang));
     }
   }
+  // suffix token t sits at span_end + t; with SIF, original token t at t and C^2
+  // token j at the position of the last token of its block
+  if (sif) {
+    p.sif_n = sif->n_tokens;
+    p.sif_block = sif->block;
+    p.sif_sink = sif->sink;
+  }
+  auto suffix_pos = [&](int b, int64_t t) -> int64_t {
+    if (!sif) return p.span_end[b] + t;
+    if (t < sif->n_tokens) return t;
+    return std::min<int64_t>((t - sif->n_tokens + 1) * sif->block, sif->n_tokens) - 1;
+  };
   float* suf_cs = reinterpret_cast<float*>(p.image.data() + w.suf_cs);
   for (int b = 0; b < B; ++b)
     for (int64_t t = 0; t < S; ++t)
       for (int i = 0; i < H; ++i) {
-        const double ang = double(p.span_end[b] + t) * theta[i];
+        const double ang = double(suffix_pos(b, t)) * theta[i];
         const size_t k = ((size_t(b) * S + t) * H + i) * 2;
         suf_cs[k + 0] = static_cast<float>(std::cos(ang));
         suf_cs[k + 1] = static_cast<float>(std::sin(ang));
       }
   return C2KV_OK;
+}
+
+c2kv_status build_sif_plan(const c2kv_attn_cfg& cfg, int32_t batch, int32_t n_tokens,
+                           int32_t block, int32_t sink, const c2kv_plan_opts* opts, Plan& p,
+                           std::string& err) {
+  if (batch < 1 || n_tokens < 1 || block < 1 || sink < 0 || sink > n_tokens) {
+    err = fmt("SIF shape: need batch >= 1, n_tokens >= 1, block >= 1, 0 <= sink <= n_tokens; got ",
+              batch, ", ", n_tokens, ", ", block, ", ", sink);
+    return C2KV_E_INVAL;
+  }
+  const int64_t m = (int64_t(n_tokens) + block - 1) / block;
+  if (n_tokens + m > kI32Max / 2) { err = "SIF sequence too long"; return C2KV_E_UNSUPPORTED; }
+  // no composed segments: the whole [original | C^2] sequence is the suffix
+  std::vector<int32_t> seg_off(size_t(batch) + 1, 0);
+  const int32_t kept_off0 = 0;
+  c2kv_compose_desc d{};
+  d.batch = batch;
+  d.n_segments = 0;
+  d.req_seg_off = seg_off.data();
+  d.seg_kept_off = &kept_off0;
+  const SifShape sif{n_tokens, block, sink};
+  return build_plan(cfg, d, static_cast<int32_t>(n_tokens + m), opts, p, err, &sif);
 }
 
 }  // namespace c2kv

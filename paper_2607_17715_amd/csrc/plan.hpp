@@ -55,6 +55,7 @@ struct Plan {
   int32_t batch = 0, suffix_len = 0, page_size = 64, n_segments = 0;
   int32_t group = 1;               // G = H_q / H_kv
   bool keys_pre_rope = false;      // pool keys stored before RoPE: per-slot cos/sin rows
+  int32_t sif_n = 0, sif_block = 0, sif_sink = 0;   // SIF mask (sif_n > 0) instead of causal
   bool pool_compressed = false;    // slot k of a segment reads row seg_row0 + k
   std::vector<std::pair<int64_t, int64_t>> load_rows;   // merged [first, end) row ranges
   float qscale_log2 = 0.f;         // softmax scale * log2(e)
@@ -91,10 +92,20 @@ struct Plan {
   size_t d_workspace_bytes = 0;
 };
 
-// Builds the plan; returns C2KV_OK or an error with `err` set.
+// Extraction-time attention with Structured Information Flow: a sequence of
+// n_tokens original tokens followed by one C^2 token per block of `block` tokens.
+struct SifShape { int32_t n_tokens, block, sink; };
+
+// Builds the plan; returns C2KV_OK or an error with `err` set.  With `sif`, the
+// request has no segments and its suffix is the SIF sequence.
 c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& desc,
                        int32_t suffix_len, const c2kv_plan_opts* opts, Plan& plan,
-                       std::string& err);
+                       std::string& err, const SifShape* sif = nullptr);
+
+// The SIF plan: batch sequences of n_tokens + ceil(n_tokens / block) tokens.
+c2kv_status build_sif_plan(const c2kv_attn_cfg& cfg, int32_t batch, int32_t n_tokens,
+                           int32_t block, int32_t sink, const c2kv_plan_opts* opts,
+                           Plan& plan, std::string& err);
 
 }  // namespace c2kv
 

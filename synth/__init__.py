@@ -286,8 +286,56 @@ def build(sp: Spec, layer: int = 0, seed: Optional[int] = None) -> Workload:
         suffix_len=S, q=q, k_suf=k_suf, v_suf=v_suf, keys_pre_rope=sp.keys_pre_rope)
 
 
+@dataclasses.dataclass
+class SifWorkload:
+    """Inputs of extraction-time SIF attention: `batch` sequences of n original
+    tokens and their ceil(n / block) C^2 tokens, before RoPE."""
+    name: str
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    rope_base: float
+    act_dtype: str
+    n_tokens: int
+    block: int
+    sink: int
+    q: np.ndarray                # [B][L][H_q][d] in the act dtype's storage
+    k: np.ndarray                # [B][L][H_kv][d]
+    v: np.ndarray
+
+    @property
+    def batch(self) -> int:
+        return int(self.q.shape[0])
+
+    @property
+    def seq_len(self) -> int:
+        return int(self.q.shape[1])
+
+
+def sif(name="sif", batch=2, n_tokens=300, block=4, sink=4, n_q_heads=8, n_kv_heads=2,
+        head_dim=128, rope_base=5e5, act_dtype="bf16", seed=BASE_SEED + 100) -> SifWorkload:
+    """Seeded N(0,1) queries, keys and values of SIF sequences."""
+    L = n_tokens + -(-n_tokens // block)
+    s_q, s_k, s_v = (np.random.Generator(np.random.PCG64(x))
+                     for x in np.random.SeedSequence(seed).spawn(3))
+    q = cast_f64(s_q.standard_normal((batch, L, n_q_heads, head_dim)), act_dtype)
+    k = cast_f64(s_k.standard_normal((batch, L, n_kv_heads, head_dim)), act_dtype)
+    v = cast_f64(s_v.standard_normal((batch, L, n_kv_heads, head_dim)), act_dtype)
+    return SifWorkload(name, n_q_heads, n_kv_heads, head_dim, rope_base, act_dtype, n_tokens,
+                       block, sink, q, k, v)
+
+
+def sif_config(name: str) -> SifWorkload:
+    """The SIF extraction workload of the benchmark: 16 Llama-3-8B-shaped document
+    chunks of 512 tokens, one C^2 token per 4 (compression 4), a 4-token sink."""
+    if name == "sif-extract-llama3-8b-bf16":
+        return sif(name, batch=16, n_tokens=512, block=4, sink=4, n_q_heads=32, n_kv_heads=8,
+                   head_dim=128, rope_base=5e5, act_dtype="bf16", seed=BASE_SEED + 12)
+    raise ValueError(name)
+
+
 def config(idx: int, layer: int = 0) -> Workload:
-    """Workload `idx` (1..5), seeded with BASE_SEED + idx."""
+    """Workload `idx` (see spec), seeded with BASE_SEED + idx."""
     return build(spec(idx), layer=layer, seed=BASE_SEED + idx)
 
 

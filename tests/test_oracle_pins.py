@@ -534,3 +534,103 @@ def test_generator_bf16_paths_agree():
     rng = np.random.default_rng(18)
     x = (rng.standard_normal(1 << 17) * 5).astype(np.float32)
     np.testing.assert_array_equal(synth.f32_to_bf16_bits(x), synth.f32_to_bf16_bits_int(x))
+
+
+# ---------------------------------------------------------------------------
+# extraction-time attention with Structured Information Flow (Section 3.3)
+# ---------------------------------------------------------------------------
+
+def test_sif_worked_example():
+    """n = 5 originals, blocks of 2, a 1-token sink: blocks {0,1}, {2,3}, {4};
+    C^2 tokens at the positions of their blocks' last tokens 1, 3, 4."""
+    np.testing.assert_array_equal(oracle.sif_positions(5, 2), [0, 1, 2, 3, 4, 1, 3, 4])
+    #               o0 o1 o2 o3 o4 c0 c1 c2
+    want = np.array([[1, 0, 0, 0, 0, 0, 0, 0],
+                     [1, 1, 0, 0, 0, 0, 0, 0],
+                     [1, 1, 1, 0, 0, 0, 0, 0],
+                     [1, 1, 1, 1, 0, 0, 0, 0],
+                     [1, 1, 1, 1, 1, 0, 0, 0],
+                     [1, 1, 0, 0, 0, 1, 0, 0],      # c0: its block {0, 1}, sink {0}
+                     [1, 0, 1, 1, 0, 1, 1, 0],      # c1: {2, 3}, sink, c0..c1
+                     [1, 0, 0, 0, 1, 1, 1, 1]], bool)
+    np.testing.assert_array_equal(oracle.sif_mask(5, 2, 1), want)
+
+
+def _sif_reference(q, k, v, n, block, sink, base):
+    """Independent construction: visible key sets per row from the definitions
+    (1-based blocks B(j) = {(j-1)k+1, ..., min(jk, n)}), C^2 positions from each
+    block's last member, complex-form RoPE, torch SDPA with the boolean mask."""
+    m = -(-n // block)
+    blocks = [list(range((j - 1) * block + 1, min(j * block, n) + 1)) for j in range(1, m + 1)]
+    pos = list(range(n)) + [max(b) - 1 for b in blocks]         # 0-based positions
+    L = n + m
+    mask = torch.zeros(L, L, dtype=torch.bool)
+    for t in range(1, n + 1):                                     # original x_t (1-based)
+        for u in range(1, t + 1):
+            mask[t - 1, u - 1] = True
+    for j in range(1, m + 1):                                     # C^2 token c_j
+        row = n + j - 1
+        for u in set(blocks[j - 1]) | set(range(1, sink + 1)):
+            mask[row, u - 1] = True
+        for jj in range(1, j + 1):
+            mask[row, n + jj - 1] = True
+    P = np.array(pos, np.float64)[:, None]
+    qp = _rope_complex(q, P, base)
+    kp = _rope_complex(k, P, base)
+    qt = torch.from_numpy(qp).permute(1, 0, 2)[None]
+    kt = torch.from_numpy(kp).permute(1, 0, 2)[None]
+    vt = torch.from_numpy(np.asarray(v, np.float64)).permute(1, 0, 2)[None]
+    o = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=mask,
+                                                         enable_gqa=True)
+    return o[0].permute(1, 0, 2).numpy()
+
+
+@pytest.mark.parametrize("n,block,sink", [(13, 4, 0), (13, 4, 2), (8, 8, 3), (9, 1, 1),
+                                          (7, 10, 7)])
+def test_sif_matches_independent_construction(n, block, sink):
+    w = synth.sif(batch=1, n_tokens=n, block=block, sink=sink, n_q_heads=4, n_kv_heads=2,
+                  head_dim=8, act_dtype="f32", seed=n * 100 + block * 10 + sink)
+    q, k, v = (x[0].astype(np.float64) for x in (w.q, w.k, w.v))
+    out, lse = oracle.sif_attend(q, k, v, n, block, sink, w.rope_base)
+    ref = _sif_reference(q, k, v, n, block, sink, w.rope_base)
+    np.testing.assert_allclose(out, ref, atol=1e-10, rtol=0)
+    assert np.isfinite(lse).all()
+
+
+def test_sif_original_token_invariance_and_locality():
+    """Original rows are plain causal attention over the originals and ignore
+    every C^2 token; a C^2 row ignores originals outside its block and the sink
+    and later C^2 tokens, and does see its own block."""
+    n, block, sink = 20, 4, 2
+    w = synth.sif(batch=1, n_tokens=n, block=block, sink=sink, n_q_heads=4, n_kv_heads=2,
+                  head_dim=8, act_dtype="f32", seed=77)
+    q, k, v = (x[0].astype(np.float64).copy() for x in (w.q, w.k, w.v))
+    out, _ = oracle.sif_attend(q, k, v, n, block, sink, w.rope_base)
+    # originals: torch causal SDPA over the first n tokens only
+    P = np.arange(n, dtype=np.float64)[:, None]
+    qt = torch.from_numpy(_rope_complex(q[:n], P, w.rope_base)).permute(1, 0, 2)[None]
+    kt = torch.from_numpy(_rope_complex(k[:n], P, w.rope_base)).permute(1, 0, 2)[None]
+    vt = torch.from_numpy(v[:n]).permute(1, 0, 2)[None]
+    causal = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, is_causal=True,
+                                                              enable_gqa=True)
+    np.testing.assert_allclose(out[:n], causal[0].permute(1, 0, 2).numpy(), atol=1e-10, rtol=0)
+    rng = np.random.default_rng(5)
+    # perturbing C^2 tokens leaves the original rows as they are
+    k2, v2 = k.copy(), v.copy()
+    k2[n:] += rng.standard_normal(k2[n:].shape)
+    v2[n:] += rng.standard_normal(v2[n:].shape)
+    o2, _ = oracle.sif_attend(q, k2, v2, n, block, sink, w.rope_base)
+    np.testing.assert_array_equal(o2[:n], out[:n])
+    # C^2 token j = 2 (block {8..11}): originals 4..7 and 12.. and C^2 tokens 3.. do not matter
+    j = 2
+    k3, v3 = k.copy(), v.copy()
+    for u in list(range(sink, j * block)) + list(range((j + 1) * block, n)) + list(range(n + j + 1, len(k))):
+        k3[u] += 1.0
+        v3[u] += 1.0
+    o3, _ = oracle.sif_attend(q, k3, v3, n, block, sink, w.rope_base)
+    np.testing.assert_allclose(o3[n + j], out[n + j], atol=1e-12, rtol=0)
+    # ...but a token of its own block does
+    v4 = v.copy()
+    v4[j * block + 1] += 1.0
+    o4, _ = oracle.sif_attend(q, k, v4, n, block, sink, w.rope_base)
+    assert np.abs(o4[n + j] - out[n + j]).max() > 1e-3
