@@ -297,7 +297,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   // and a second round of workgroups.
   const bool split = int64_t(groups.size()) < target;
   const int64_t per_item =
-      split ? std::max<int64_t>(2, (total_tiles + target - 1) / target) : INT32_MAX;
+      split ? std::max<int64_t>(1, (total_tiles + target - 1) / target) : INT32_MAX;
   std::vector<WorkItem> items;
   for (const Group& gr : groups) {
     // splits of each range, at most kMaxSplits in all
