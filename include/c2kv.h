@@ -42,7 +42,8 @@
  *   k_pages         [n_pages][H_kv][page_size][D]   act dtype, keys at final positions
  *   v_pages         [n_pages][H_kv][D][page_size]   act dtype, values, TRANSPOSED in a page
  *   A request's composed slot s lives in page block_table[b][s / page_size] at
- *   offset s % page_size.
+ *   offset s % page_size; a request's pages are consecutive
+ *   (block_table[b][i] = block_table[b][0] + i).
  *
  * Semantics (the readings of the paper this library implements)
  *   - Stored keys carry RoPE at their original positions orig_pos0 + j; compose

@@ -383,7 +383,7 @@ struct TileLoader {
   static constexpr int KUPK = D / 16;       // key units per key
 
   const AttnParams& a;
-  const int tid, b, g, S, slot0, N, nct;
+  const int tid, b, g, S, slot0, N, nct, page0;
   const int kp2;                            // first of the two keys of this thread's value units
   const T* ksuf;
   const T* vsuf;
@@ -393,70 +393,86 @@ struct TileLoader {
   uint32_t rk[Sh::RKW], rv[Sh::RVW];
   float ck[Sh::NKU][8], sk[Sh::NKU][8];     // cos/sin of this thread's key units
   int cs_seg[Sh::NKU];                      // segment the pool cos/sin belong to
-  int2 nk[Sh::NKU], nv[2];                  // (row, segment) of the next tile's keys
+  int2 nk[Sh::NKU];                         // (row, segment) of the next tile's keys
+  int nv[2];                                // pool rows of its values (only the row: a
+                                            // loaded word left unused would be reused
+                                            // while its load is in flight)
+  bool nk_ok[Sh::NKU], nv_ok[2];            // which of them are inside the tile
   int n_page = 0;
   bool k_ok[Sh::NKU];
   bool v_ok[2];
   float k_scale[Sh::NKU], v_scale[2];
 
   __device__ __forceinline__ TileLoader(const AttnParams& a_, int tid_, int b_, int g_, int slot0_,
-                                        int N_)
+                                        int N_, int page0_)
       : a(a_), tid(tid_), b(b_), g(g_), S(a_.S), slot0(slot0_), N(N_), nct((N_ + KT - 1) / KT),
+        page0(page0_),
         kp2(2 * (tid_ % (KT / 2))), ksuf(static_cast<const T*>(a_.k_suf)),
         vsuf(static_cast<const T*>(a_.v_suf)), kpool(static_cast<const PoolT*>(a_.k)),
         vpool(static_cast<const PoolT*>(a_.v)) {
 #pragma unroll
     for (int i = 0; i < Sh::NKU; ++i) {
-      nk[i] = make_int2(-1, -1);
+      nk[i] = make_int2(0, -1);
+      nk_ok[i] = false;
       cs_seg[i] = -1;
       k_ok[i] = false;
       k_scale[i] = 1.f;
     }
-    nv[0] = nv[1] = make_int2(-1, -1);
+    nv[0] = nv[1] = 0;
+    nv_ok[0] = nv_ok[1] = false;
     v_ok[0] = v_ok[1] = false;
     v_scale[0] = v_scale[1] = 1.f;
   }
 
+  // Every load here and in fetch_data is unconditional, from a clamped index
+  // inside the tile (validity is kept apart): a load whose destination was
+  // first set to a default would make the compiler wait for all loads in
+  // flight, including the row loads of the tile after next.
+  // SUF: the tile is a suffix tile (tile >= nct), known at compile time so
+  // that a loop runs one kind of tile and its loads have one set of registers.
+  template <bool SUF>
   __device__ __forceinline__ void fetch_idx(int tile) {
-    if (tile >= nct) return;                // suffix tiles need no index
+    if constexpr (SUF) return;              // suffix tiles need no index
     const int k0 = tile * KT;
-    const int nvalid = min(KT, N - k0);
+    const int nvalid = min(KT, N - k0);     // >= 1 for a cached tile
     if constexpr (kPaged) {
-      n_page = a.block_table[size_t(b) * a.max_pages + k0 / a.PS];
+      // a request's pages are consecutive: no table read (a scalar load in
+      // flight would turn every LDS operand wait of the tile into a full wait)
+      n_page = page0 + k0 / a.PS;
     } else {
 #pragma unroll
       for (int i = 0; i < Sh::NKU; ++i) {
         const int u = tid + i * NT;
         const int kk = u / KUPK;
-        nk[i] = make_int2(-1, -1);
-        if (u < Sh::KU_TOT && kk < nvalid) nk[i] = a.slot_info[slot0 + k0 + kk];
+        nk_ok[i] = u < Sh::KU_TOT && kk < nvalid;
+        nk[i] = a.slot_info[slot0 + k0 + min(kk, nvalid - 1)];
       }
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        nv[j] = make_int2(-1, -1);
-        if (kp2 + j < nvalid) nv[j] = a.slot_info[slot0 + k0 + kp2 + j];
+        nv_ok[j] = kp2 + j < nvalid;
+        nv[j] = a.slot_info[slot0 + k0 + min(kp2 + j, nvalid - 1)].x;
       }
     }
   }
 
+  template <bool SUF>
   __device__ __forceinline__ void fetch_data(int tile) {
-    const bool suffix = tile >= nct;
-    const int k0 = suffix ? (tile - nct) * KT : tile * KT;
-    const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
-    if (suffix) {
+    const int k0 = SUF ? (tile - nct) * KT : tile * KT;
+    const int nvalid = SUF ? min(KT, S - k0) : min(KT, N - k0);   // >= 1
+    if constexpr (SUF) {
 #pragma unroll
       for (int i = 0; i < Sh::NKU; ++i) {
         const int u = tid + i * NT;
         const int kk = u / KUPK, c = u % KUPK;
         uint32_t* w = rk + i * 2 * Sh::WA;
         k_ok[i] = u < Sh::KU_TOT && kk < nvalid;
-        if (k_ok[i]) {
-          const size_t tok = size_t(b) * S + k0 + kk;
+        if (u < Sh::KU_TOT) {                 // uniform per wavefront
+          const size_t tok = size_t(b) * S + k0 + min(kk, nvalid - 1);
           const size_t row = tok * a.Hkv + g;
           raw_load8<T>(w, ksuf + row * D + 8 * c);
           raw_load8<T>(w + Sh::WA, ksuf + row * D + 8 * c + HALF);
           load_cs8(a.suf_cs + tok * HALF + 8 * c, ck[i], sk[i]);
-          cs_seg[i] = -1;                   // not a pool segment's cos/sin
+          cs_seg[i] = -1;                     // not a pool segment's cos/sin
         }
       }
 #pragma unroll
@@ -467,8 +483,8 @@ struct TileLoader {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           v_ok[j] = u < Sh::VU_TOT && kp2 + j < nvalid;
-          if (v_ok[j]) {
-            const size_t row = (size_t(b) * S + k0 + kp2 + j) * a.Hkv + g;
+          if (u < Sh::VU_TOT) {
+            const size_t row = (size_t(b) * S + k0 + min(kp2 + j, nvalid - 1)) * a.Hkv + g;
             raw_load8<T>(w + j * Sh::WA, vsuf + row * D + 8 * c);
           }
         }
@@ -482,20 +498,20 @@ struct TileLoader {
 #pragma unroll
       for (int i = 0; i < Sh::NPK; ++i) {
         const int u = tid + i * NT;
-        const int kk = u / (D / EPV), vec = u % (D / EPV);
-        uint4 val = make_uint4(0u, 0u, 0u, 0u);
-        if (u < Sh::PK_TOT && kk < nvalid)
-          val = *reinterpret_cast<const uint4*>(kpage + size_t(kk) * D + vec * EPV);
-        rk[4 * i] = val.x; rk[4 * i + 1] = val.y; rk[4 * i + 2] = val.z; rk[4 * i + 3] = val.w;
+        const int kk = min(u / (D / EPV), nvalid - 1), vec = u % (D / EPV);
+        if (u < Sh::PK_TOT) {
+          const uint4 val = *reinterpret_cast<const uint4*>(kpage + size_t(kk) * D + vec * EPV);
+          rk[4 * i] = val.x; rk[4 * i + 1] = val.y; rk[4 * i + 2] = val.z; rk[4 * i + 3] = val.w;
+        }
       }
 #pragma unroll
       for (int i = 0; i < Sh::NPV; ++i) {
         const int u = tid + i * NT;
-        const int d = u / (KT / EPV), vec = u % (KT / EPV);
-        uint4 val = make_uint4(0u, 0u, 0u, 0u);
-        if (u < Sh::PV_TOT && vec * EPV < nvalid)
-          val = *reinterpret_cast<const uint4*>(vpage + size_t(d) * a.PS + vec * EPV);
-        rv[4 * i] = val.x; rv[4 * i + 1] = val.y; rv[4 * i + 2] = val.z; rv[4 * i + 3] = val.w;
+        const int d = u / (KT / EPV), vec = min(u % (KT / EPV), (nvalid - 1) / EPV);
+        if (u < Sh::PV_TOT) {
+          const uint4 val = *reinterpret_cast<const uint4*>(vpage + size_t(d) * a.PS + vec * EPV);
+          rv[4 * i] = val.x; rv[4 * i + 1] = val.y; rv[4 * i + 2] = val.z; rv[4 * i + 3] = val.w;
+        }
       }
     } else {
 #pragma unroll
@@ -503,8 +519,8 @@ struct TileLoader {
         const int u = tid + i * NT;
         const int c = u % KUPK;
         uint32_t* w = rk + i * 2 * Sh::WP;
-        k_ok[i] = nk[i].x >= 0;
-        if (k_ok[i]) {
+        k_ok[i] = nk_ok[i];
+        if (u < Sh::KU_TOT) {
           const size_t row = size_t(nk[i].x) * a.Hkv + g;
           raw_load8<PoolT>(w, kpool + row * D + 8 * c);
           raw_load8<PoolT>(w + Sh::WP, kpool + row * D + 8 * c + HALF);
@@ -522,9 +538,9 @@ struct TileLoader {
         uint32_t* w = rv + i * 2 * Sh::WP;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          v_ok[j] = u < Sh::VU_TOT && nv[j].x >= 0;
-          if (v_ok[j]) {
-            const size_t row = size_t(nv[j].x) * a.Hkv + g;
+          v_ok[j] = u < Sh::VU_TOT && nv_ok[j];
+          if (u < Sh::VU_TOT) {
+            const size_t row = size_t(nv[j]) * a.Hkv + g;
             raw_load8<PoolT>(w + j * Sh::WP, vpool + row * D + 8 * c);
             if constexpr (SRC == SRC_POOL_I8) v_scale[j] = a.v_scale[row];
           }
@@ -533,12 +549,12 @@ struct TileLoader {
     }
   }
 
+  template <bool SUF>
   __device__ __forceinline__ void commit(int tile, T* sK, T* sV) {
-    const bool suffix = tile >= nct;
-    const int k0 = suffix ? (tile - nct) * KT : tile * KT;
-    const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
-    if (suffix || !kPaged) {
-      const bool from_pool = !suffix;
+    const int k0 = SUF ? (tile - nct) * KT : tile * KT;
+    const int nvalid = SUF ? min(KT, S - k0) : min(KT, N - k0);
+    if (SUF || !kPaged) {
+      constexpr bool from_pool = !SUF;
 #pragma unroll
       for (int i = 0; i < Sh::NKU; ++i) {
         const int u = tid + i * NT;
@@ -676,10 +692,10 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
   const int t = row_ok ? r / G : 0;
   const int h = g * G + (row_ok ? r % G : 0);
 
-  TileLoader<T, D, SRC, NT> ld(a, tid, b, g, slot0, N);
-  auto fetch_idx = [&](int tile) { ld.fetch_idx(tile); };
-  auto fetch_data = [&](int tile) { ld.fetch_data(tile); };
-  auto commit = [&](int tile, T* sK, T* sV) { ld.commit(tile, sK, sV); };
+  TileLoader<T, D, SRC, NT> ld(a, tid, b, g, slot0, N, it.page0);
+  // suffix tiles (tile >= nct) and cached tiles run in loops of their own
+  const int t0 = it.tile0, t1 = it.tile1;
+  const int tc = min(t1, nct);             // cached tiles [t0, tc), suffix [max(t0, nct), t1)
 
   // ---- Q operand: RoPE at span_end + t, softmax scale and log2(e) folded in.
   // Lane (qi, half) holds d = c*KSTEP + half*KPL + e in qop[c][e]; the RoPE
@@ -687,8 +703,7 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
   // The Q and cos/sin loads are issued first, then the first key tile's row
   // loads (whose addresses wait only for the slot indices), and only then is Q
   // rotated, so the two latencies overlap.
-  const int t0 = it.tile0, t1 = it.tile1;
-  fetch_idx(t0);
+  if (t0 < nct) ld.template fetch_idx<false>(t0);
   Op qop[NQC];
   {
     const T* qrow = static_cast<const T*>(a.q) + ((size_t(b) * S + t) * a.Hq + h) * D;
@@ -713,7 +728,8 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
         }
       }
     }
-    fetch_data(t0);
+    if (t0 < nct) ld.template fetch_data<false>(t0);
+    else ld.template fetch_data<true>(t0);
 #pragma unroll
     for (int c = 0; c < NQC / 2; ++c) {
       float x[KPL], y[KPL];
@@ -905,64 +921,74 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
     }
   };
 
-  // prologue: tile t0 (loads issued above) into stage 0, tile t0 + 1 in registers
-  if (t0 + 1 < t1) fetch_idx(t0 + 1);
-  commit(t0, kst(0), vst(0));
-  if (t0 + 1 < t1) fetch_data(t0 + 1);
-  if (t0 + 2 < t1) fetch_idx(t0 + 2);
-  __syncthreads();
+  // Tiles [ta, tb) of one kind.  Prologue: tile ta (its loads issued already
+  // when `fetched`) into stage 0, tile ta + 1 in registers.  The loads of a
+  // run's first tile cannot be issued under the previous run's last tile: a
+  // load of the other kind anywhere in the loop would make the compiler's
+  // waits there conservative again.
+  auto run_tiles = [&](auto suf_c, int ta, int tb, bool fetched) {
+    constexpr bool SUF = decltype(suf_c)::value;
+    if (ta >= tb) return;
+    if (!fetched) ld.template fetch_data<SUF>(ta);
+    if (ta + 1 < tb) ld.template fetch_idx<SUF>(ta + 1);
+    ld.template commit<SUF>(ta, kst(0), vst(0));
+    if (ta + 1 < tb) ld.template fetch_data<SUF>(ta + 1);
+    if (ta + 2 < tb) ld.template fetch_idx<SUF>(ta + 2);
+    __syncthreads();
+    for (int tile = ta; tile < tb; ++tile) {
+      const int stage = (tile - ta) & 1;
+      // next tile into the other stage; its readers finished before the last barrier
+      if (tile + 1 < tb) {
+        ld.template commit<SUF>(tile + 1, kst(stage ^ 1), vst(stage ^ 1));
+        if (tile + 2 < tb) ld.template fetch_data<SUF>(tile + 2);
+        if (tile + 3 < tb) ld.template fetch_idx<SUF>(tile + 3);
+      }
+      f32x16 s[NKB];
+      qk(kst(stage), s);
+      const float m_new = mask_max(tile, s);
+      const float m_ref = (m_new == kNegInf) ? 0.f : m_new;
+      if constexpr (KPL == 8) {
+        // bf16: the reference maximum moves only when some row's maximum outgrows it
+        // by more than kLazyLog2 (a factor 2^kLazyLog2), so the output rescale is
+        // rare; probabilities stay below 2^kLazyLog2, which bf16 and fp32 sums hold
+        if (__any(m_new > m_run + kLazyLog2)) rescale(m_new, m_ref);
+        Op pb[NPW];
+        l_run += exp_pack(s, m_run == kNegInf ? 0.f : m_run, pb);
+        pv(vst(stage), pb);
+      } else {
+        float psum = 0.f;
+#pragma unroll
+        for (int j = 0; j < NKB; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float p = __builtin_amdgcn_exp2f(s[j][v] - m_ref);
+            s[j][v] = p;
+            psum += p;
+          }
+        rescale(m_new, m_ref);
+        l_run += psum;
 
-  for (int tile = t0; tile < t1; ++tile) {
-    const int stage = (tile - t0) & 1;
-    // next tile into the other stage; its readers finished before the last barrier
-    if (tile + 1 < t1) {
-      commit(tile + 1, kst(stage ^ 1), vst(stage ^ 1));
-      if (tile + 2 < t1) fetch_data(tile + 2);
-      if (tile + 3 < t1) fetch_idx(tile + 3);
-    }
-    f32x16 s[NKB];
-    qk(kst(stage), s);
-    const float m_new = mask_max(tile, s);
-    const float m_ref = (m_new == kNegInf) ? 0.f : m_new;
-    if constexpr (KPL == 8) {
-      // bf16: the reference maximum moves only when some row's maximum outgrows it
-      // by more than kLazyLog2 (a factor 2^kLazyLog2), so the output rescale is
-      // rare; probabilities stay below 2^kLazyLog2, which bf16 and fp32 sums hold
-      if (__any(m_new > m_run + kLazyLog2)) rescale(m_new, m_ref);
-      Op pb[NPW];
-      l_run += exp_pack(s, m_run == kNegInf ? 0.f : m_run, pb);
-      pv(vst(stage), pb);
-    } else {
-      float psum = 0.f;
+        // ---- O^T += V^T P^T with fp32 MFMA: chunk c takes accumulator value
+        // v0 = c % CPB of block c / CPB (key 8*(v0/4) + 4*half + v0%4 of it)
+        const T* sV = vst(stage);
 #pragma unroll
-      for (int j = 0; j < NKB; ++j)
+        for (int cc = 0; cc < NPC / KG; ++cc) {
+          const int c = kh * (NPC / KG) + cc;
+          const int j = cc / CPB;
+          const int kb = c / CPB;
+          const int v0 = KPL * (c % CPB);
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float p = __builtin_amdgcn_exp2f(s[j][v] - m_ref);
-          s[j][v] = p;
-          psum += p;
-        }
-      rescale(m_new, m_ref);
-      l_run += psum;
-
-      // ---- O^T += V^T P^T with fp32 MFMA: chunk c takes accumulator value
-      // v0 = c % CPB of block c / CPB (key 8*(v0/4) + 4*half + v0%4 of it)
-      const T* sV = vst(stage);
-#pragma unroll
-      for (int cc = 0; cc < NPC / KG; ++cc) {
-        const int c = kh * (NPC / KG) + cc;
-        const int j = cc / CPB;
-        const int kb = c / CPB;
-        const int v0 = KPL * (c % CPB);
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          const T* vrow = sV + (db * 32 + qi) * L::LDV + kb * 32 + 4 * half;
-          o[db] = M::run(vrow[8 * (v0 >> 2) + (v0 & 3)], s[j][v0], o[db]);
+          for (int db = 0; db < NDB; ++db) {
+            const T* vrow = sV + (db * 32 + qi) * L::LDV + kb * 32 + 4 * half;
+            o[db] = M::run(vrow[8 * (v0 >> 2) + (v0 & 3)], s[j][v0], o[db]);
+          }
         }
       }
+      __syncthreads();   // next stage written; this stage free for the tile after next
     }
-    __syncthreads();   // next stage written; this stage free for the tile after next
-  }
+  };
+  run_tiles(std::false_type{}, t0, tc, true);
+  run_tiles(std::true_type{}, max(t0, nct), t1, t0 >= nct);
 
   // ---- the two key halves of a row group combine (same lane, same rows)
   if constexpr (KG == 2) {

@@ -325,7 +325,8 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
         const int32_t t0 = first + static_cast<int32_t>(int64_t(len) * s / nsr[ri]);
         const int32_t t1 = first + static_cast<int32_t>(int64_t(len) * (s + 1) / nsr[ri]);
         items.push_back({gr.b, gr.g, gr.row0, gr.nrows, t0, t1, ns > 1 ? part0 + k : -1, merge,
-                         p.req_slot0[gr.b], p.req_slot0[gr.b + 1] - p.req_slot0[gr.b], 0, 0});
+                         p.req_slot0[gr.b], p.req_slot0[gr.b + 1] - p.req_slot0[gr.b],
+                         p.block_table[size_t(gr.b) * p.max_pages], 0});
       }
     }
   }

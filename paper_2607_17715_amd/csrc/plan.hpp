@@ -24,7 +24,8 @@ constexpr int kRowsPerWave = 32;    // query rows one wavefront owns (MFMA 32-wi
 // otherwise write partial `partial` of merge group `merge`.
 struct WorkItem {
   int32_t b, g, row0, nrows, tile0, tile1, partial, merge;
-  int32_t slot0, nslots, pad0, pad1;   // request b's composed slots [slot0, slot0 + nslots)
+  int32_t slot0, nslots;               // request b's composed slots [slot0, slot0 + nslots)
+  int32_t page0, pad1;                 // request b's first page (its pages are consecutive)
 };
 
 // Row block whose key splits are combined by the merge kernel.
