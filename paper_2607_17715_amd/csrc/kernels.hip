@@ -31,6 +31,9 @@ constexpr int KT = kKeyTile;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLazyLog2 = 8.f;  // reference-maximum slack of the bf16 online softmax
 constexpr float kLn2 = 0.693147180559945309f;
+// fourth descriptor word of a raw (unformatted, unswizzled) buffer on gfx9-family
+// parts; reads past num_records return zero
+constexpr int kBufferFlags = 0x00020000;
 
 enum Src { SRC_PAGED = 0, SRC_POOL = 1, SRC_POOL_I8 = 2 };
 
@@ -398,6 +401,7 @@ struct TileLoader {
                                             // loaded word left unused would be reused
                                             // while its load is in flight)
   bool nk_ok[Sh::NKU], nv_ok[2];            // which of them are inside the tile
+  uint32_t kofs[Sh::NPK], vofs[Sh::NPV];    // paged: byte offsets of this thread's vectors
   int n_page = 0;
   bool k_ok[Sh::NKU];
   bool v_ok[2];
@@ -420,6 +424,19 @@ struct TileLoader {
     }
     nv[0] = nv[1] = 0;
     nv_ok[0] = nv_ok[1] = false;
+    if constexpr (kPaged) {
+      constexpr int EPV = Sh::EPV;
+#pragma unroll
+      for (int i = 0; i < Sh::NPK; ++i) {
+        const int u = tid + i * NT;
+        kofs[i] = uint32_t((u / (D / EPV)) * D + (u % (D / EPV)) * EPV) * sizeof(T);
+      }
+#pragma unroll
+      for (int i = 0; i < Sh::NPV; ++i) {
+        const int u = tid + i * NT;
+        vofs[i] = uint32_t((u / (KT / EPV)) * a.PS + (u % (KT / EPV)) * EPV) * sizeof(T);
+      }
+    }
     v_ok[0] = v_ok[1] = false;
     v_scale[0] = v_scale[1] = 1.f;
   }
@@ -490,27 +507,30 @@ struct TileLoader {
         }
       }
     } else if constexpr (kPaged) {
-      constexpr int EPV = Sh::EPV;
+      // buffer loads: the descriptors are this tile's key block and transposed
+      // value block (scalar arithmetic), the per-thread offsets never change.
+      // Rows or columns past nvalid are read as they lie in the page (keys are
+      // masked, values zeroed at commit); nothing outside the tile is read.
       const size_t ph = size_t(n_page) * a.Hkv + g;
       const int off = k0 % a.PS;
-      const T* kpage = static_cast<const T*>(a.k) + (ph * a.PS + off) * D;
-      const T* vpage = static_cast<const T*>(a.v) + ph * D * a.PS + off;
+      const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<T*>(static_cast<const T*>(a.k) + (ph * a.PS + off) * D), 0,
+          KT * D * int(sizeof(T)), kBufferFlags);
+      const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<T*>(static_cast<const T*>(a.v) + ph * D * a.PS + off), 0,
+          ((D - 1) * a.PS + KT) * int(sizeof(T)), kBufferFlags);
 #pragma unroll
       for (int i = 0; i < Sh::NPK; ++i) {
-        const int u = tid + i * NT;
-        const int kk = min(u / (D / EPV), nvalid - 1), vec = u % (D / EPV);
-        if (u < Sh::PK_TOT) {
-          const uint4 val = *reinterpret_cast<const uint4*>(kpage + size_t(kk) * D + vec * EPV);
-          rk[4 * i] = val.x; rk[4 * i + 1] = val.y; rk[4 * i + 2] = val.z; rk[4 * i + 3] = val.w;
+        if (tid + i * NT < Sh::PK_TOT) {
+          const auto val = __builtin_amdgcn_raw_buffer_load_b128(kr, kofs[i], 0, 0);
+          rk[4 * i] = val[0]; rk[4 * i + 1] = val[1]; rk[4 * i + 2] = val[2]; rk[4 * i + 3] = val[3];
         }
       }
 #pragma unroll
       for (int i = 0; i < Sh::NPV; ++i) {
-        const int u = tid + i * NT;
-        const int d = u / (KT / EPV), vec = min(u % (KT / EPV), (nvalid - 1) / EPV);
-        if (u < Sh::PV_TOT) {
-          const uint4 val = *reinterpret_cast<const uint4*>(vpage + size_t(d) * a.PS + vec * EPV);
-          rv[4 * i] = val.x; rv[4 * i + 1] = val.y; rv[4 * i + 2] = val.z; rv[4 * i + 3] = val.w;
+        if (tid + i * NT < Sh::PV_TOT) {
+          const auto val = __builtin_amdgcn_raw_buffer_load_b128(vr, vofs[i], 0, 0);
+          rv[4 * i] = val[0]; rv[4 * i + 1] = val[1]; rv[4 * i + 2] = val[2]; rv[4 * i + 3] = val[3];
         }
       }
     } else {
@@ -635,7 +655,7 @@ struct TileLoader {
         if (u >= Sh::PV_TOT) continue;
         const int d = u / (KT / EPV), vec = u % (KT / EPV);
         uint4 val = make_uint4(rv[4 * i], rv[4 * i + 1], rv[4 * i + 2], rv[4 * i + 3]);
-        if (vec * EPV + EPV > nvalid) val = keep_first<T>(val, nvalid - vec * EPV);
+        if (nvalid < KT && vec * EPV + EPV > nvalid) val = keep_first<T>(val, nvalid - vec * EPV);
         uint2* dst = reinterpret_cast<uint2*>(sV + d * L::LDV + vec * EPV);   // 8-byte aligned rows
         dst[0] = make_uint2(val.x, val.y);
         dst[1] = make_uint2(val.z, val.w);
