@@ -581,7 +581,7 @@ struct TileLoader {
         if (u >= Sh::KU_TOT) continue;
         const int kk = u / KUPK, c = u % KUPK;
         T* dst = sK + kk * L::LDK + 8 * c;
-        if (!k_ok[i]) {
+        if (nvalid < KT && !k_ok[i]) {        // only a partial tile has such keys
           store8_zero(dst);
           store8_zero(dst + HALF);
           continue;
@@ -611,6 +611,20 @@ struct TileLoader {
         const int u = tid + i * NT;
         if (u >= Sh::VU_TOT) continue;
         const int c = u / (KT / 2);
+        // bf16 values that need no decode: a transposed word holds element e of
+        // the two keys kp2 and kp2 + 1, i.e. one 16-bit half of each row's word
+        constexpr bool kRawV = sizeof(T) == 2 && !(from_pool && SRC == SRC_POOL_I8);
+        if (kRawV && nvalid == KT) {
+          const uint32_t* w0 = rv + i * 2 * (from_pool ? Sh::WP : Sh::WA);
+          const uint32_t* w1 = w0 + (from_pool ? Sh::WP : Sh::WA);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            T* dst = sV + (8 * c + e) * L::LDV + kp2;
+            *reinterpret_cast<uint32_t*>(dst) =
+                __builtin_amdgcn_perm(w1[e / 2], w0[e / 2], (e & 1) ? 0x07060302u : 0x05040100u);
+          }
+          continue;
+        }
         float x0[8], x1[8];
         if (from_pool) {
           if constexpr (!kPaged) {
