@@ -394,6 +394,7 @@ struct TileLoader {
   const PoolT* vpool;
 
   uint32_t rk[Sh::RKW], rv[Sh::RVW];
+  uint32_t rk2[Sh::RKW], rv2[Sh::RVW];      // paged: a second tile in flight
   float ck[Sh::NKU][8], sk[Sh::NKU][8];     // cos/sin of this thread's key units
   int cs_seg[Sh::NKU];                      // segment the pool cos/sin belong to
   int2 nk[Sh::NKU];                         // (row, segment) of the next tile's keys
@@ -402,7 +403,6 @@ struct TileLoader {
                                             // while its load is in flight)
   bool nk_ok[Sh::NKU], nv_ok[2];            // which of them are inside the tile
   uint32_t kofs[Sh::NPK], vofs[Sh::NPV];    // paged: byte offsets of this thread's vectors
-  int n_page = 0;
   bool k_ok[Sh::NKU];
   bool v_ok[2];
   float k_scale[Sh::NKU], v_scale[2];
@@ -453,9 +453,9 @@ struct TileLoader {
     const int k0 = tile * KT;
     const int nvalid = min(KT, N - k0);     // >= 1 for a cached tile
     if constexpr (kPaged) {
-      // a request's pages are consecutive: no table read (a scalar load in
-      // flight would turn every LDS operand wait of the tile into a full wait)
-      n_page = page0 + k0 / a.PS;
+      // a request's pages are consecutive: the page is page0 + k0 / PS, no table
+      // read (a scalar load in flight would turn every LDS operand wait of the
+      // tile into a full wait)
     } else {
 #pragma unroll
       for (int i = 0; i < Sh::NKU; ++i) {
@@ -470,6 +470,69 @@ struct TileLoader {
         nv[j] = a.slot_info[slot0 + k0 + min(kp2 + j, nvalid - 1)].x;
       }
     }
+  }
+
+  // Paged tiles: buffer loads whose descriptors are this tile's key block and
+  // transposed value block (scalar arithmetic); the per-thread offsets never
+  // change.  Rows or columns past nvalid are read as they lie in the page
+  // (keys are masked, values zeroed at commit); nothing outside the tile is read.
+  // With `real` false the descriptors have no extent: the loads return zeros and
+  // touch no memory, but still count, so a loop issues the same loads each turn.
+  __device__ __forceinline__ void paged_fetch(int k0, uint32_t (&K)[Sh::RKW],
+                                              uint32_t (&V)[Sh::RVW], bool real = true) {
+    const size_t ph = size_t(page0 + k0 / a.PS) * a.Hkv + g;
+    const int off = k0 % a.PS;
+    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(static_cast<const T*>(a.k) + (ph * a.PS + off) * D), 0,
+        real ? KT * D * int(sizeof(T)) : 0, kBufferFlags);
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(static_cast<const T*>(a.v) + ph * D * a.PS + off), 0,
+        real ? ((D - 1) * a.PS + KT) * int(sizeof(T)) : 0, kBufferFlags);
+    static_assert(Sh::PK_TOT % NT == 0 && Sh::PV_TOT % NT == 0,
+                  "every thread loads whole page vectors");
+#pragma unroll
+    for (int i = 0; i < Sh::NPK; ++i) {
+      const auto val = __builtin_amdgcn_raw_buffer_load_b128(kr, kofs[i], 0, 0);
+      K[4 * i] = val[0]; K[4 * i + 1] = val[1]; K[4 * i + 2] = val[2]; K[4 * i + 3] = val[3];
+    }
+#pragma unroll
+    for (int i = 0; i < Sh::NPV; ++i) {
+      const auto val = __builtin_amdgcn_raw_buffer_load_b128(vr, vofs[i], 0, 0);
+      V[4 * i] = val[0]; V[4 * i + 1] = val[1]; V[4 * i + 2] = val[2]; V[4 * i + 3] = val[3];
+    }
+  }
+  __device__ __forceinline__ void paged_commit(int k0, const uint32_t (&K)[Sh::RKW],
+                                               const uint32_t (&V)[Sh::RVW], T* sK, T* sV) {
+    constexpr int EPV = Sh::EPV;
+    const int nvalid = min(KT, N - k0);
+#pragma unroll
+    for (int i = 0; i < Sh::NPK; ++i) {
+      const int u = tid + i * NT;
+      const int kk = u / (D / EPV), vec = u % (D / EPV);
+      *reinterpret_cast<uint4*>(sK + kk * L::LDK + vec * EPV) =
+          make_uint4(K[4 * i], K[4 * i + 1], K[4 * i + 2], K[4 * i + 3]);
+    }
+#pragma unroll
+    for (int i = 0; i < Sh::NPV; ++i) {
+      const int u = tid + i * NT;
+      const int d = u / (KT / EPV), vec = u % (KT / EPV);
+      uint4 val = make_uint4(V[4 * i], V[4 * i + 1], V[4 * i + 2], V[4 * i + 3]);
+      if (nvalid < KT && vec * EPV + EPV > nvalid) val = keep_first<T>(val, nvalid - vec * EPV);
+      uint2* dst = reinterpret_cast<uint2*>(sV + d * L::LDV + vec * EPV);   // 8-byte aligned rows
+      dst[0] = make_uint2(val.x, val.y);
+      dst[1] = make_uint2(val.z, val.w);
+    }
+  }
+  // cached paged tile `tile` into / out of register set B
+  template <int B>
+  __device__ __forceinline__ void fetch_set(int tile, bool real) {
+    if constexpr (B == 0) paged_fetch(tile * KT, rk, rv, real);
+    else paged_fetch(tile * KT, rk2, rv2, real);
+  }
+  template <int B>
+  __device__ __forceinline__ void commit_set(int tile, T* sK, T* sV) {
+    if constexpr (B == 0) paged_commit(tile * KT, rk, rv, sK, sV);
+    else paged_commit(tile * KT, rk2, rv2, sK, sV);
   }
 
   template <bool SUF>
@@ -507,32 +570,7 @@ struct TileLoader {
         }
       }
     } else if constexpr (kPaged) {
-      // buffer loads: the descriptors are this tile's key block and transposed
-      // value block (scalar arithmetic), the per-thread offsets never change.
-      // Rows or columns past nvalid are read as they lie in the page (keys are
-      // masked, values zeroed at commit); nothing outside the tile is read.
-      const size_t ph = size_t(n_page) * a.Hkv + g;
-      const int off = k0 % a.PS;
-      const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<T*>(static_cast<const T*>(a.k) + (ph * a.PS + off) * D), 0,
-          KT * D * int(sizeof(T)), kBufferFlags);
-      const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<T*>(static_cast<const T*>(a.v) + ph * D * a.PS + off), 0,
-          ((D - 1) * a.PS + KT) * int(sizeof(T)), kBufferFlags);
-#pragma unroll
-      for (int i = 0; i < Sh::NPK; ++i) {
-        if (tid + i * NT < Sh::PK_TOT) {
-          const auto val = __builtin_amdgcn_raw_buffer_load_b128(kr, kofs[i], 0, 0);
-          rk[4 * i] = val[0]; rk[4 * i + 1] = val[1]; rk[4 * i + 2] = val[2]; rk[4 * i + 3] = val[3];
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < Sh::NPV; ++i) {
-        if (tid + i * NT < Sh::PV_TOT) {
-          const auto val = __builtin_amdgcn_raw_buffer_load_b128(vr, vofs[i], 0, 0);
-          rv[4 * i] = val[0]; rv[4 * i + 1] = val[1]; rv[4 * i + 2] = val[2]; rv[4 * i + 3] = val[3];
-        }
-      }
+      paged_fetch(k0, rk, rv);
     } else {
 #pragma unroll
       for (int i = 0; i < Sh::NKU; ++i) {
@@ -654,26 +692,7 @@ struct TileLoader {
         }
       }
     } else {
-      constexpr int EPV = Sh::EPV;
-#pragma unroll
-      for (int i = 0; i < Sh::NPK; ++i) {
-        const int u = tid + i * NT;
-        if (u >= Sh::PK_TOT) continue;
-        const int kk = u / (D / EPV), vec = u % (D / EPV);
-        *reinterpret_cast<uint4*>(sK + kk * L::LDK + vec * EPV) =
-            make_uint4(rk[4 * i], rk[4 * i + 1], rk[4 * i + 2], rk[4 * i + 3]);
-      }
-#pragma unroll
-      for (int i = 0; i < Sh::NPV; ++i) {
-        const int u = tid + i * NT;
-        if (u >= Sh::PV_TOT) continue;
-        const int d = u / (KT / EPV), vec = u % (KT / EPV);
-        uint4 val = make_uint4(rv[4 * i], rv[4 * i + 1], rv[4 * i + 2], rv[4 * i + 3]);
-        if (nvalid < KT && vec * EPV + EPV > nvalid) val = keep_first<T>(val, nvalid - vec * EPV);
-        uint2* dst = reinterpret_cast<uint2*>(sV + d * L::LDV + vec * EPV);   // 8-byte aligned rows
-        dst[0] = make_uint2(val.x, val.y);
-        dst[1] = make_uint2(val.z, val.w);
-      }
+      paged_commit(k0, rk, rv, sK, sV);
     }
   }
 };
@@ -960,65 +979,106 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
   // run's first tile cannot be issued under the previous run's last tile: a
   // load of the other kind anywhere in the loop would make the compiler's
   // waits there conservative again.
-  auto run_tiles = [&](auto suf_c, int ta, int tb, bool fetched) {
-    constexpr bool SUF = decltype(suf_c)::value;
-    if (ta >= tb) return;
-    if (!fetched) ld.template fetch_data<SUF>(ta);
-    if (ta + 1 < tb) ld.template fetch_idx<SUF>(ta + 1);
-    ld.template commit<SUF>(ta, kst(0), vst(0));
-    if (ta + 1 < tb) ld.template fetch_data<SUF>(ta + 1);
-    if (ta + 2 < tb) ld.template fetch_idx<SUF>(ta + 2);
-    __syncthreads();
-    for (int tile = ta; tile < tb; ++tile) {
-      const int stage = (tile - ta) & 1;
-      // next tile into the other stage; its readers finished before the last barrier
-      if (tile + 1 < tb) {
-        ld.template commit<SUF>(tile + 1, kst(stage ^ 1), vst(stage ^ 1));
-        if (tile + 2 < tb) ld.template fetch_data<SUF>(tile + 2);
-        if (tile + 3 < tb) ld.template fetch_idx<SUF>(tile + 3);
-      }
-      f32x16 s[NKB];
-      qk(kst(stage), s);
-      const float m_new = mask_max(tile, s);
-      const float m_ref = (m_new == kNegInf) ? 0.f : m_new;
-      if constexpr (KPL == 8) {
-        // bf16: the reference maximum moves only when some row's maximum outgrows it
-        // by more than kLazyLog2 (a factor 2^kLazyLog2), so the output rescale is
-        // rare; probabilities stay below 2^kLazyLog2, which bf16 and fp32 sums hold
-        if (__any(m_new > m_run + kLazyLog2)) rescale(m_new, m_ref);
-        Op pb[NPW];
-        l_run += exp_pack(s, m_run == kNegInf ? 0.f : m_run, pb);
-        pv(vst(stage), pb);
-      } else {
-        float psum = 0.f;
+  // ---- one key tile in LDS stage `stage`: scores, online softmax, P*V
+  auto tile_compute = [&](int tile, int stage) __attribute__((always_inline)) {
+    f32x16 s[NKB];
+    qk(kst(stage), s);
+    const float m_new = mask_max(tile, s);
+    const float m_ref = (m_new == kNegInf) ? 0.f : m_new;
+    if constexpr (KPL == 8) {
+      // bf16: the reference maximum moves only when some row's maximum outgrows it
+      // by more than kLazyLog2 (a factor 2^kLazyLog2), so the output rescale is
+      // rare; probabilities stay below 2^kLazyLog2, which bf16 and fp32 sums hold
+      if (__any(m_new > m_run + kLazyLog2)) rescale(m_new, m_ref);
+      Op pb[NPW];
+      l_run += exp_pack(s, m_run == kNegInf ? 0.f : m_run, pb);
+      pv(vst(stage), pb);
+    } else {
+      float psum = 0.f;
 #pragma unroll
-        for (int j = 0; j < NKB; ++j)
+      for (int j = 0; j < NKB; ++j)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float p = __builtin_amdgcn_exp2f(s[j][v] - m_ref);
-            s[j][v] = p;
-            psum += p;
-          }
-        rescale(m_new, m_ref);
-        l_run += psum;
+        for (int v = 0; v < 16; ++v) {
+          const float p = __builtin_amdgcn_exp2f(s[j][v] - m_ref);
+          s[j][v] = p;
+          psum += p;
+        }
+      rescale(m_new, m_ref);
+      l_run += psum;
 
-        // ---- O^T += V^T P^T with fp32 MFMA: chunk c takes accumulator value
-        // v0 = c % CPB of block c / CPB (key 8*(v0/4) + 4*half + v0%4 of it)
-        const T* sV = vst(stage);
+      // ---- O^T += V^T P^T with fp32 MFMA: chunk c takes accumulator value
+      // v0 = c % CPB of block c / CPB (key 8*(v0/4) + 4*half + v0%4 of it)
+      const T* sV = vst(stage);
 #pragma unroll
-        for (int cc = 0; cc < NPC / KG; ++cc) {
-          const int c = kh * (NPC / KG) + cc;
-          const int j = cc / CPB;
-          const int kb = c / CPB;
-          const int v0 = KPL * (c % CPB);
+      for (int cc = 0; cc < NPC / KG; ++cc) {
+        const int c = kh * (NPC / KG) + cc;
+        const int j = cc / CPB;
+        const int kb = c / CPB;
+        const int v0 = KPL * (c % CPB);
 #pragma unroll
-          for (int db = 0; db < NDB; ++db) {
-            const T* vrow = sV + (db * 32 + qi) * L::LDV + kb * 32 + 4 * half;
-            o[db] = M::run(vrow[8 * (v0 >> 2) + (v0 & 3)], s[j][v0], o[db]);
-          }
+        for (int db = 0; db < NDB; ++db) {
+          const T* vrow = sV + (db * 32 + qi) * L::LDV + kb * 32 + 4 * half;
+          o[db] = M::run(vrow[8 * (v0 >> 2) + (v0 & 3)], s[j][v0], o[db]);
         }
       }
-      __syncthreads();   // next stage written; this stage free for the tile after next
+    }
+  };
+
+  // in the paged loop below, a wavefront whose row group is empty (decode: 4
+  // rows in a 128-row block) still loads and commits its share of each tile
+  // but computes nothing
+  const bool rows_here = rgrp * 32 < it.nrows;
+
+  // bf16 pages with 128-row blocks (short suffixes, decode: bandwidth-bound) keep
+  // two tiles' loads in flight, in two register sets that alternate
+  constexpr bool kDeep = kPaged && KG == 2 && sizeof(T) == 2;
+
+  // Tiles [ta, tb) of one kind.  Prologue: tile ta (its loads issued already
+  // when `fetched`) into stage 0, tile ta + 1 in registers.  The loads of a
+  // run's first tile cannot be issued under the previous run's last tile: a
+  // load of the other kind anywhere in the loop would make the compiler's
+  // waits there conservative again.
+  auto run_tiles = [&](auto suf_c, int ta, int tb, bool fetched) __attribute__((always_inline)) {
+    constexpr bool SUF = decltype(suf_c)::value;
+    if (ta >= tb) return;
+    if constexpr (!SUF && kDeep) {
+      // tile ta's loads are in set 0; tile t's set is (t - ta) & 1.  Every turn
+      // issues its loads unconditionally (no-extent descriptors past the end),
+      // so that the commits wait only for their own set.
+      ld.template fetch_set<1>(ta + 1, ta + 1 < tb);
+      ld.template commit_set<0>(ta, kst(0), vst(0));
+      ld.template fetch_set<0>(ta + 2, ta + 2 < tb);
+      __syncthreads();
+      auto step = [&](auto nb_c, int tile) __attribute__((always_inline)) {
+        constexpr int NB = decltype(nb_c)::value;   // register set of tile + 1
+        const int stage = (tile - ta) & 1;
+        if (tile + 1 < tb) ld.template commit_set<NB>(tile + 1, kst(stage ^ 1), vst(stage ^ 1));
+        ld.template fetch_set<NB>(tile + 3, tile + 3 < tb);
+        if (tile < tb && rows_here) tile_compute(tile, stage);
+        __syncthreads();   // next stage written; this stage free for the tile after next
+      };
+      for (int tile = ta; tile < tb; tile += 2) {
+        step(std::integral_constant<int, 1>{}, tile);
+        step(std::integral_constant<int, 0>{}, tile + 1);
+      }
+    } else {
+      if (!fetched) ld.template fetch_data<SUF>(ta);
+      if (ta + 1 < tb) ld.template fetch_idx<SUF>(ta + 1);
+      ld.template commit<SUF>(ta, kst(0), vst(0));
+      if (ta + 1 < tb) ld.template fetch_data<SUF>(ta + 1);
+      if (ta + 2 < tb) ld.template fetch_idx<SUF>(ta + 2);
+      __syncthreads();
+      for (int tile = ta; tile < tb; ++tile) {
+        const int stage = (tile - ta) & 1;
+        // next tile into the other stage; its readers finished before the last barrier
+        if (tile + 1 < tb) {
+          ld.template commit<SUF>(tile + 1, kst(stage ^ 1), vst(stage ^ 1));
+          if (tile + 2 < tb) ld.template fetch_data<SUF>(tile + 2);
+          if (tile + 3 < tb) ld.template fetch_idx<SUF>(tile + 3);
+        }
+        tile_compute(tile, stage);
+        __syncthreads();   // next stage written; this stage free for the tile after next
+      }
     }
   };
   run_tiles(std::false_type{}, t0, tc, true);
