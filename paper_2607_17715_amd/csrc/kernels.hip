@@ -35,7 +35,10 @@ constexpr float kLn2 = 0.693147180559945309f;
 // parts; reads past num_records return zero
 constexpr int kBufferFlags = 0x00020000;
 
-enum Src { SRC_PAGED = 0, SRC_POOL = 1, SRC_POOL_I8 = 2 };
+// SRC_PAGED_SIF: pages, with the Structured Information Flow mask over the
+// suffix instead of the causal one (its own kernels, so that the causal ones
+// carry none of the SIF mask's registers)
+enum Src { SRC_PAGED = 0, SRC_POOL = 1, SRC_POOL_I8 = 2, SRC_PAGED_SIF = 3 };
 
 // ----------------------------------------------------------------------------
 // element helpers
@@ -305,15 +308,31 @@ struct Shape {
   static constexpr int RVW = imax(NVU * 2 * WA, PAGED ? NPV * 4 : NVU * 2 * WP);
 };
 
-// Structured Information Flow mask over the sequence [n originals | C^2 tokens]:
-// an original sees earlier originals; C^2 token j sees the originals of its
-// block, the sink (the first sif_sink originals) and C^2 tokens 0..j.
-__device__ inline bool sif_visible(int t, int u, const AttnParams& a) {
-  if (t < a.sif_n) return u <= t;
-  const int j = t - a.sif_n;
-  if (u >= a.sif_n) return u - a.sif_n <= j;
-  return u < a.sif_sink || u / a.sif_block == j;
-}
+// The suffix keys a query row sees, as ranges fixed per row.  Causal: keys
+// [0, t].  Structured Information Flow over the sequence [n originals | C^2
+// tokens]: an original t sees originals [0, t]; C^2 token j = t - n sees C^2
+// tokens [n, t], the sink [0, sif_sink) and the originals of its block
+// [j*block, min((j+1)*block, n)).
+struct RowKeys {
+  int lo, hi;          // [lo, hi], inclusive
+  int sink;            // [0, sink)
+  int blo, bhi;        // [blo, bhi)
+  __device__ RowKeys(int t, const AttnParams& a) {
+    lo = 0; hi = t; sink = 0; blo = 0; bhi = 0;
+    if (a.sif_n > 0 && t >= a.sif_n) {
+      const int j = t - a.sif_n;
+      lo = a.sif_n;
+      sink = a.sif_sink;
+      blo = j * a.sif_block;
+      bhi = min((j + 1) * a.sif_block, a.sif_n);
+    }
+  }
+  // each range test is one unsigned compare of u - start against the length
+  __device__ bool sees(int u) const {
+    return unsigned(u - lo) <= unsigned(hi - lo) || u < sink ||
+           unsigned(u - blo) < unsigned(bhi - blo);
+  }
+};
 
 // ----------------------------------------------------------------------------
 // log-sum-exp combine of the key splits of one row block (rows [rlo, rhi))
@@ -379,7 +398,7 @@ __device__ inline void merge_rows(const MergeGroup& mg, int rlo, int rhi, const 
 template <typename T, int D, int SRC, int NT>
 struct TileLoader {
   using PoolT = typename std::conditional<SRC == SRC_POOL_I8, int8_t, T>::type;
-  static constexpr bool kPaged = SRC == SRC_PAGED;
+  static constexpr bool kPaged = SRC == SRC_PAGED || SRC == SRC_PAGED_SIF;
   using Sh = Shape<T, PoolT, D, NT, kPaged>;
   using L = Lds<T, D>;
   static constexpr int HALF = D / 2;
@@ -710,7 +729,8 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
   using Op = typename M::Op;
   using L = Lds<T, D>;
   using PoolT = typename std::conditional<SRC == SRC_POOL_I8, int8_t, T>::type;
-  constexpr bool kPaged = SRC == SRC_PAGED;
+  constexpr bool kPaged = SRC == SRC_PAGED || SRC == SRC_PAGED_SIF;
+  constexpr bool kSif = SRC == SRC_PAGED_SIF;
   using Sh = Shape<T, PoolT, D, NT, kPaged>;
   constexpr int KPL = M::KPL;
   constexpr int KSTEP = 2 * KPL;            // contraction length of one MFMA
@@ -875,14 +895,14 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
     const int k0 = suffix ? (tile - nct) * KT : tile * KT;
     const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
     if (suffix || nvalid < KT) {
+      const RowKeys row_keys(t, a);        // SIF kernels only (unused otherwise)
 #pragma unroll
       for (int j = 0; j < NKB; ++j)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int key = (kh * NKB + j) * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
           const int u = k0 + key;
-          const bool vis = key < nvalid && (!suffix || (a.sif_n > 0 ? sif_visible(t, u, a)
-                                                                      : u <= t));
+          const bool vis = key < nvalid && (!suffix || (kSif ? row_keys.sees(u) : u <= t));
           if (!vis) s[j][v] = kNegInf;
         }
     }
@@ -1450,6 +1470,12 @@ hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const vo
   const int n = static_cast<int>(p.items.size());
   const int rows = p.rows_per_block;      // selects the row-block shape
   const int D = p.cfg.head_dim;
+  // a SIF plan has no cached tiles: its kernels never read k / v, whatever they are
+  if (p.sif_n > 0) {
+    if (p.cfg.act_dtype == C2KV_F32)
+      return launch_attn_d<float, SRC_PAGED_SIF>(D, ap, n, rows, st, e0, e1);
+    return launch_attn_d<__bf16, SRC_PAGED_SIF>(D, ap, n, rows, st, e0, e1);
+  }
   if (p.cfg.act_dtype == C2KV_F32) {
     if (src_kind == SRC_PAGED) return launch_attn_d<float, SRC_PAGED>(D, ap, n, rows, st, e0, e1);
     return launch_attn_d<float, SRC_POOL>(D, ap, n, rows, st, e0, e1);
