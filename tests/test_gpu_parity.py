@@ -77,6 +77,19 @@ def test_decode_128k_4x():
     _both_paths(synth.config(7), "decode-128k-4x")
 
 
+@pytest.mark.parametrize("suffix_len", [1, 7, 25])
+@pytest.mark.parametrize("opts", [dict(kv_splits=1), dict(kv_splits=2), dict(kv_splits=3),
+                                  dict(kv_splits=5), dict(kv_splits=3, page_size=128)])
+def test_paged_128_row_blocks_tile_counts(suffix_len, opts):
+    """128-row blocks over pages keep two tiles in flight in alternating register
+    sets, so an item's tile count may be odd or even, and its first and last
+    tiles partial; with few suffix tokens most 32-row groups hold no rows."""
+    w = synth.small(batch=3, n_q_heads=16, n_kv_heads=4, suffix_len=suffix_len,
+                    chunks_per_req=3, keep=("ratio", 0.2, 0.9))
+    plan = _both_paths(w, f"paged-128 S={suffix_len} {opts}", rows_per_block=128, **opts)
+    assert plan.info["rows_per_block"] == 128
+
+
 # ---------------------------------------------------------------------------
 # keys stored before RoPE; C^2-pattern kept sets at compression 4 / 8 / 10 / 16
 # ---------------------------------------------------------------------------
