@@ -34,6 +34,9 @@ constexpr float kLn2 = 0.693147180559945309f;
 // fourth descriptor word of a raw (unformatted, unswizzled) buffer on gfx9-family
 // parts; reads past num_records return zero
 constexpr int kBufferFlags = 0x00020000;
+// row blocks (of at most 128 rows) with more splits than this are merged one
+// row per workgroup
+constexpr int kSplitMergeMin = 16;
 
 // SRC_PAGED_SIF: pages, with the Structured Information Flow mask over the
 // suffix instead of the causal one (its own kernels, so that the causal ones
@@ -716,14 +719,15 @@ struct TileLoader {
   }
 };
 
-// One workgroup = 8 wavefronts.  With KG = 1 each wavefront owns 32 query rows
-// (256 per workgroup) and every key of a tile; with KG = 2 four row groups of
-// 32 rows (128 per workgroup) each see one half of every 64-key tile, keep their
-// own online softmax, and the two halves are combined through LDS at the end.
-template <typename T, int D, int SRC, int KG>
-__global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
-  constexpr int NT = 512;
-  constexpr int NRG = 8 / KG;               // row groups
+// One workgroup = NT / 64 wavefronts.  With KG = 1 each wavefront owns 32 query
+// rows (256 per 512-thread workgroup) and every key of a tile; with KG = 2 row
+// groups of 32 rows (128 rows per 512 threads, 64 per 256) each see one half of
+// every 64-key tile, keep their own online softmax, and the two halves are
+// combined through LDS at the end.  256-thread workgroups (64-row blocks) run two
+// to a CU, so that two work items' latencies overlap.
+template <typename T, int D, int SRC, int KG, int NT>
+__global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
+  constexpr int NRG = NT / 64 / KG;         // row groups
   constexpr int NKB = 2 / KG;               // 32-key blocks per wavefront and tile
   using M = Mma<T>;
   using Op = typename M::Op;
@@ -1051,7 +1055,7 @@ __global__ __launch_bounds__(512, 2) void attn_kernel(AttnParams a) {
 
   // bf16 pages with 128-row blocks (short suffixes, decode: bandwidth-bound) keep
   // two tiles' loads in flight, in two register sets that alternate
-  constexpr bool kDeep = kPaged && KG == 2 && sizeof(T) == 2;
+  constexpr bool kDeep = kPaged && KG == 2 && NT == 512 && sizeof(T) == 2;
 
   // Tiles [ta, tb) of one kind.  Prologue: tile ta (its loads issued already
   // when `fetched`) into stage 0, tile ta + 1 in registers.  The loads of a
@@ -1302,6 +1306,99 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
     a.lse[(size_t(mg.b) * a.Hq + h) * a.S + t] = z > 0.f ? mx + __logf(z) : kNegInf;
 }
 
+// One row per workgroup, the splits spread over SPL split lanes of TPR threads
+// (row blocks with few rows and many splits: decode, short suffixes).  Each
+// thread reads its splits' LSEs and partial elements in one batch of loads; the
+// maximum, the sum of weights and the weighted rows are reduced across lanes
+// through LDS.  SPB splits per lane per batch.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void merge_split_kernel(MergeParams a) {
+  constexpr int EPT = 4;
+  constexpr int TPR = D / EPT;                 // threads per row
+  constexpr int SPL = 256 / TPR;               // split lanes
+  constexpr int SPB = 8;                       // splits per lane per batch
+  __shared__ float s_red[256];
+  __shared__ float s_acc[SPL][D];
+  const MergeGroup mg = a.groups[blockIdx.x];
+  const int rloc = blockIdx.y;
+  if (rloc >= mg.nrows) return;
+  const int tid = threadIdx.x, sl = tid / TPR, sub = tid % TPR;
+  const int last = mg.nsplit - 1;
+  const float* pl = a.part_lse + size_t(mg.part0) * a.RB + rloc;
+  const T* po = static_cast<const T*>(a.part_o) + (size_t(mg.part0) * a.RB + rloc) * D + sub * EPT;
+
+  // maximum over all split LSEs: every thread reads the splits of its lane
+  float mx = kNegInf;
+  for (int i0 = sl; i0 <= last; i0 += SPL * SPB) {
+    float l[SPB];
+#pragma unroll
+    for (int k = 0; k < SPB; ++k) l[k] = pl[size_t(min(i0 + k * SPL, last)) * a.RB];
+#pragma unroll
+    for (int k = 0; k < SPB; ++k) mx = fmaxf(mx, i0 + k * SPL <= last ? l[k] : kNegInf);
+  }
+  s_red[tid] = mx;
+  __syncthreads();
+  mx = kNegInf;
+#pragma unroll 8
+  for (int i = 0; i < 256; i += TPR) mx = fmaxf(mx, s_red[i]);
+  __syncthreads();
+
+  // weighted partial rows of this lane's splits
+  float z = 0.f, acc[EPT] = {};
+  for (int i0 = sl; i0 <= last; i0 += SPL * SPB) {
+    float l[SPB], v[SPB][EPT];
+#pragma unroll
+    for (int k = 0; k < SPB; ++k) {
+      const int i = min(i0 + k * SPL, last);
+      l[k] = pl[size_t(i) * a.RB];
+      const T* src = po + size_t(i) * a.RB * D;
+      if constexpr (sizeof(T) == 4) {
+        const float4 x = *reinterpret_cast<const float4*>(src);
+        v[k][0] = x.x; v[k][1] = x.y; v[k][2] = x.z; v[k][3] = x.w;
+      } else {
+        const uint2 u = *reinterpret_cast<const uint2*>(src);
+        v[k][0] = __uint_as_float(u.x << 16);
+        v[k][1] = __uint_as_float(u.x & 0xffff0000u);
+        v[k][2] = __uint_as_float(u.y << 16);
+        v[k][3] = __uint_as_float(u.y & 0xffff0000u);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < SPB; ++k) {
+      const float w = (i0 + k * SPL <= last && l[k] != kNegInf) ? __expf(l[k] - mx) : 0.f;
+      z += w;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) acc[e] += w * v[k][e];
+    }
+  }
+  // lane sums: z from the sub == 0 thread of each lane, the rows element-wise
+  s_red[tid] = z;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) s_acc[sl][sub * EPT + e] = acc[e];
+  __syncthreads();
+  if (sl != 0) return;
+  float zt = 0.f;
+#pragma unroll
+  for (int j = 0; j < SPL; ++j) zt += s_red[j * TPR];
+  float o[EPT] = {};
+#pragma unroll
+  for (int j = 0; j < SPL; ++j)
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) o[e] += s_acc[j][sub * EPT + e];
+  const float inv = zt > 0.f ? 1.f / zt : 0.f;
+  const int r = mg.row0 + rloc;
+  const int t = r / a.G, h = mg.g * a.G + r % a.G;
+  T* orow = static_cast<T*>(a.out) + ((size_t(mg.b) * a.S + t) * a.Hq + h) * D + sub * EPT;
+  if constexpr (sizeof(T) == 4) {
+    *reinterpret_cast<float4*>(orow) = make_float4(o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
+  } else {
+    *reinterpret_cast<uint2*>(orow) =
+        make_uint2(pack_bf16(o[0] * inv, o[1] * inv), pack_bf16(o[2] * inv, o[3] * inv));
+  }
+  if (a.lse && sub == 0)
+    a.lse[(size_t(mg.b) * a.Hq + h) * a.S + t] = zt > 0.f ? mx + __logf(zt) : kNegInf;
+}
+
 // ----------------------------------------------------------------------------
 // compose: gather -> decode -> turn -> paged write
 // ----------------------------------------------------------------------------
@@ -1415,8 +1512,11 @@ T* at_mut(void* base, size_t off) {
 template <typename T, int D, int SRC>
 hipError_t launch_attn_t(const AttnParams& ap, int n_items, int rows, hipStream_t st,
                          hipEvent_t e0, hipEvent_t e1) {
-  const void* k = rows == 256 ? reinterpret_cast<const void*>(&attn_kernel<T, D, SRC, 1>)
-                              : reinterpret_cast<const void*>(&attn_kernel<T, D, SRC, 2>);
+  if (rows == 64)
+    return launch(reinterpret_cast<const void*>(&attn_kernel<T, D, SRC, 2, 256>), dim3(n_items),
+                  dim3(256), st, ap, e0, e1);
+  const void* k = rows == 256 ? reinterpret_cast<const void*>(&attn_kernel<T, D, SRC, 1, 512>)
+                              : reinterpret_cast<const void*>(&attn_kernel<T, D, SRC, 2, 512>);
   return launch(k, dim3(n_items), dim3(512), st, ap, e0, e1);
 }
 
@@ -1499,6 +1599,19 @@ hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st, hi
   mp.out = out;
   mp.lse = lse;
   const int D = p.cfg.head_dim;
+  if (p.max_splits > kSplitMergeMin && p.rows_per_block <= 128) {
+    // many splits over few rows: one workgroup per row, splits spread over lanes
+    // (256-row blocks have rows enough to fill the machine with 8 rows a group)
+    const dim3 grid(static_cast<unsigned>(p.merges.size()), p.rows_per_block);
+    const void* k;
+    if (p.cfg.act_dtype == C2KV_F32)
+      k = D == 64 ? reinterpret_cast<const void*>(&merge_split_kernel<float, 64>)
+                  : reinterpret_cast<const void*>(&merge_split_kernel<float, 128>);
+    else
+      k = D == 64 ? reinterpret_cast<const void*>(&merge_split_kernel<__bf16, 64>)
+                  : reinterpret_cast<const void*>(&merge_split_kernel<__bf16, 128>);
+    return launch(k, grid, dim3(256), st, mp, e0, e1);
+  }
   const int rpw = 256 / (D / 4);
   const dim3 grid(static_cast<unsigned>(p.merges.size()), (p.rows_per_block + rpw - 1) / rpw);
   const void* k;

@@ -78,8 +78,9 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
     err = fmt("page_size must be a positive multiple of ", kKeyTile, ", got ", o.page_size);
     return C2KV_E_INVAL;
   }
-  if (o.rows_per_block != 0 && o.rows_per_block != 128 && o.rows_per_block != 256) {
-    err = fmt("rows_per_block must be 0, 128 or 256, got ", o.rows_per_block);
+  if (o.rows_per_block != 0 && o.rows_per_block != 64 && o.rows_per_block != 128 &&
+      o.rows_per_block != 256) {
+    err = fmt("rows_per_block must be 0, 64, 128 or 256, got ", o.rows_per_block);
     return C2KV_E_INVAL;
   }
   if (o.kv_splits < 0 || o.num_cus < 0) {
@@ -245,9 +246,10 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   const int64_t G = p.group, S = suffix_len;
   const int64_t R = G * S;            // query rows per (request, kv-head)
   int RB = o.rows_per_block;
-  if (RB == 0) RB = R >= 256 ? 256 : 128;
+  if (RB == 0) RB = R >= 256 ? 256 : R > 64 ? 128 : 64;
   p.rows_per_block = RB;
-  const int wgs_per_cu = 1;           // 8 wavefronts at 2 per SIMD fill a CU
+  // 8 wavefronts at 2 per SIMD fill a CU; 64-row blocks have 4 and run two to a CU
+  const int wgs_per_cu = RB == 64 ? 2 : 1;
   const int64_t target = int64_t(o.num_cus) * wgs_per_cu;
   const int32_t n_rb = ceil_div(R, RB);
   // A group is one row block of one (request, kv-head) and the key tiles it reads

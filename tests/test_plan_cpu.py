@@ -105,7 +105,7 @@ def test_workspace_and_work_list_sizes():
         i = plan.info
         assert i["workspace_bytes"] > 0 and i["workspace_bytes"] % 256 == 0
         assert i["n_work_items"] >= i["n_merge_groups"]
-        assert i["rows_per_block"] in (128, 256)
+        assert i["rows_per_block"] in (64, 128, 256)
     # forced split count is honoured
     w = synth.config(2)
     assert c2kv.Plan.for_workload(w, kv_splits=1).info["n_merge_groups"] == 0
@@ -138,7 +138,8 @@ def test_validation_errors():
     _expect_status(E.C2KV_E_INVAL, mk(rope_base=-1.0))
     _expect_status(E.C2KV_E_INVAL, mk(page_size=100))
     _expect_status(E.C2KV_E_INVAL, mk(rows_per_block=48))
-    _expect_status(E.C2KV_E_INVAL, mk(rows_per_block=64))
+    _expect_status(E.C2KV_E_INVAL, mk(rows_per_block=96))
+    mk(rows_per_block=64)()                                         # 64-row blocks are valid
     _expect_status(E.C2KV_E_INVAL, mk(merge_mode=3))
     mk(keys_pre_rope=True)()                                        # the other key encoding
     bad = w.kept_idx.copy()
