@@ -773,6 +773,21 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   // suffix tiles (tile >= nct) and cached tiles run in loops of their own
   const int t0 = it.tile0, t1 = it.tile1;
   const int tc = min(t1, nct);             // cached tiles [t0, tc), suffix [max(t0, nct), t1)
+  // tile at item position i: the identity, except for multi-range items of SIF
+  // plans, whose positions run through up to three ranges of suffix tiles
+  auto tile_of = [&](int i) -> int {
+    if constexpr (kSif) {
+      if (it.n_ranges > 0) {
+#pragma unroll
+        for (int r = 0; r < 3; ++r) {
+          const int first = it.rng[r] & 0xffff, len = (it.rng[r] >> 16) - first;
+          if (i < len) return first + i;
+          i -= len;
+        }
+      }
+    }
+    return i;
+  };
 
   // ---- Q operand: RoPE at span_end + t, softmax scale and log2(e) folded in.
   // Lane (qi, half) holds d = c*KSTEP + half*KPL + e in qop[c][e]; the RoPE
@@ -806,7 +821,7 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
       }
     }
     if (t0 < nct) ld.template fetch_data<false>(t0);
-    else ld.template fetch_data<true>(t0);
+    else ld.template fetch_data<true>(tile_of(t0));
 #pragma unroll
     for (int c = 0; c < NQC / 2; ++c) {
       float x[KPL], y[KPL];
@@ -1086,21 +1101,22 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         step(std::integral_constant<int, 0>{}, tile + 1);
       }
     } else {
-      if (!fetched) ld.template fetch_data<SUF>(ta);
-      if (ta + 1 < tb) ld.template fetch_idx<SUF>(ta + 1);
-      ld.template commit<SUF>(ta, kst(0), vst(0));
-      if (ta + 1 < tb) ld.template fetch_data<SUF>(ta + 1);
-      if (ta + 2 < tb) ld.template fetch_idx<SUF>(ta + 2);
+      // (positions i run through tiles tile_of(i))
+      if (!fetched) ld.template fetch_data<SUF>(tile_of(ta));
+      if (ta + 1 < tb) ld.template fetch_idx<SUF>(tile_of(ta + 1));
+      ld.template commit<SUF>(tile_of(ta), kst(0), vst(0));
+      if (ta + 1 < tb) ld.template fetch_data<SUF>(tile_of(ta + 1));
+      if (ta + 2 < tb) ld.template fetch_idx<SUF>(tile_of(ta + 2));
       __syncthreads();
-      for (int tile = ta; tile < tb; ++tile) {
-        const int stage = (tile - ta) & 1;
+      for (int i = ta; i < tb; ++i) {
+        const int stage = (i - ta) & 1;
         // next tile into the other stage; its readers finished before the last barrier
-        if (tile + 1 < tb) {
-          ld.template commit<SUF>(tile + 1, kst(stage ^ 1), vst(stage ^ 1));
-          if (tile + 2 < tb) ld.template fetch_data<SUF>(tile + 2);
-          if (tile + 3 < tb) ld.template fetch_idx<SUF>(tile + 3);
+        if (i + 1 < tb) {
+          ld.template commit<SUF>(tile_of(i + 1), kst(stage ^ 1), vst(stage ^ 1));
+          if (i + 2 < tb) ld.template fetch_data<SUF>(tile_of(i + 2));
+          if (i + 3 < tb) ld.template fetch_idx<SUF>(tile_of(i + 3));
         }
-        tile_compute(tile, stage);
+        tile_compute(tile_of(i), stage);
         __syncthreads();   // next stage written; this stage free for the tile after next
       }
     }

@@ -302,6 +302,19 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       split ? std::max<int64_t>(1, (total_tiles + target - 1) / target) : INT32_MAX;
   std::vector<WorkItem> items;
   for (const Group& gr : groups) {
+    // a SIF row block over several key ranges is one item that runs through
+    // them in turn (no partials, no merge), when its tiles fit 16-bit fields
+    if (sif && gr.ranges.size() > 1 && gr.ranges.size() <= 3 &&
+        gr.ranges.back().second < 65536 && o.kv_splits == 0) {
+      WorkItem w{gr.b, gr.g, gr.row0, gr.nrows, 0, gr.tiles, -1, -1,
+                 p.req_slot0[gr.b], p.req_slot0[gr.b + 1] - p.req_slot0[gr.b],
+                 p.block_table[size_t(gr.b) * p.max_pages], int32_t(gr.ranges.size()),
+                 {0, 0, 0}, 0};
+      for (size_t ri = 0; ri < gr.ranges.size(); ++ri)
+        w.rng[ri] = gr.ranges[ri].first | (gr.ranges[ri].second << 16);
+      items.push_back(w);
+      continue;
+    }
     // splits of each range, at most kMaxSplits in all
     std::vector<int32_t> nsr;
     int32_t ns = 0;
@@ -328,7 +341,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
         const int32_t t1 = first + static_cast<int32_t>(int64_t(len) * (s + 1) / nsr[ri]);
         items.push_back({gr.b, gr.g, gr.row0, gr.nrows, t0, t1, ns > 1 ? part0 + k : -1, merge,
                          p.req_slot0[gr.b], p.req_slot0[gr.b + 1] - p.req_slot0[gr.b],
-                         p.block_table[size_t(gr.b) * p.max_pages], 0});
+                         p.block_table[size_t(gr.b) * p.max_pages], 0, {0, 0, 0}, 0});
       }
     }
   }

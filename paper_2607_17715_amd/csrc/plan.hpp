@@ -25,7 +25,10 @@ constexpr int kRowsPerWave = 32;    // query rows one wavefront owns (MFMA 32-wi
 struct WorkItem {
   int32_t b, g, row0, nrows, tile0, tile1, partial, merge;
   int32_t slot0, nslots;               // request b's composed slots [slot0, slot0 + nslots)
-  int32_t page0, pad1;                 // request b's first page (its pages are consecutive)
+  int32_t page0;                       // request b's first page (its pages are consecutive)
+  int32_t n_ranges;                    // 0: tiles [tile0, tile1); else item position
+  int32_t rng[3];                      // i < tile1 runs through ranges [first, end) given
+  int32_t pad;                         // as first | end << 16 (multi-range SIF items)
 };
 
 // Row block whose key splits are combined by the merge kernel.

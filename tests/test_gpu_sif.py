@@ -55,7 +55,8 @@ def test_sif_matches_oracle(case):
     compare(w, out, lse, ref_out, ref_lse, what=f"sif-{case}")
 
 
-@pytest.mark.parametrize("opts", [dict(rows_per_block=128), dict(kv_splits=2),
+@pytest.mark.parametrize("opts", [dict(rows_per_block=128), dict(rows_per_block=64),
+                                  dict(rows_per_block=256), dict(kv_splits=2),
                                   dict(rows_per_block=128, kv_splits=3)])
 def test_sif_launch_shapes_agree(opts):
     w = synth.sif(batch=2, n_tokens=300, block=4, sink=4, n_q_heads=8, n_kv_heads=2, seed=950)

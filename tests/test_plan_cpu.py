@@ -196,3 +196,15 @@ def test_calls_need_an_uploaded_plan():
     assert st == c2kv.C2KV_E_WORKSPACE                              # too small
     st = lib.c2kv_plan_upload(plan.handle, ctypes.c_void_p(100), 1 << 40, None)
     assert st == c2kv.C2KV_E_WORKSPACE                              # misaligned
+
+
+def test_sif_row_blocks_need_no_merge():
+    """A SIF row block that sees several key ranges (sink, own block, original
+    tokens) is one work item running through them: with a row block per CU and
+    more, nothing is split or merged; forced splits still merge."""
+    w = synth.sif(batch=4, n_tokens=512, block=4, sink=4, n_q_heads=32, n_kv_heads=8, seed=950)
+    for rb in (64, 128, 256):
+        i = c2kv.Plan.for_sif(w, rows_per_block=rb).info
+        assert i["n_merge_groups"] == 0 and i["max_splits"] == 1, (rb, i)
+    i = c2kv.Plan.for_sif(w, kv_splits=2).info
+    assert i["n_merge_groups"] > 0 and i["max_splits"] >= 2
