@@ -765,9 +765,12 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   const int rgrp = wave % NRG, kh = wave / NRG;
   const int rloc = rgrp * 32 + qi;
   const bool row_ok = rloc < it.nrows;
-  const int r = it.row0 + rloc;
-  const int t = row_ok ? r / G : 0;
-  const int h = g * G + (row_ok ? r % G : 0);
+  // a lane past the block's last row reads that row (its result is never
+  // stored), so that every load is unconditional: a skipped load would leave
+  // the compiler's wait counts conservative for everything issued before it
+  const int r = it.row0 + min(rloc, it.nrows - 1);
+  const int t = r / G;
+  const int h = g * G + r % G;
 
   TileLoader<T, D, SRC, NT> ld(a, tid, b, g, slot0, N, it.page0);
   // suffix tiles (tile >= nct) and cached tiles run in loops of their own
@@ -794,10 +797,13 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   // partner d + D/2 sits in chunk c + NQC/2 of the same lane.
   // The Q and cos/sin loads are issued first, then the first key tile's row
   // loads (whose addresses wait only for the slot indices), and only then is Q
-  // rotated, so the two latencies overlap.
-  if (t0 < nct) ld.template fetch_idx<false>(t0);
+  // rotated, so the two latencies overlap.  The two kinds of first tile take
+  // copies of their own: where both kinds' loads could precede one wait, the
+  // compiler counts the other kind's loads in flight too.
   Op qop[NQC];
-  {
+  auto q_prologue = [&](auto suf_c) __attribute__((always_inline)) {
+    constexpr bool SUF = decltype(suf_c)::value;
+    if constexpr (!SUF) ld.template fetch_idx<false>(t0);
     const T* qrow = static_cast<const T*>(a.q) + ((size_t(b) * S + t) * a.Hq + h) * D;
     const float2* cs = a.suf_cs + (size_t(b) * S + t) * HALF;
     constexpr int NW = KPL == 8 ? 4 : 1;                 // raw words per KPL elements
@@ -806,42 +812,34 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 #pragma unroll
     for (int c = 0; c < NQC / 2; ++c) {
       const int d0 = c * KSTEP + half * KPL;
-      if (row_ok) {
-        if constexpr (KPL == 8) {
-          raw_load8<T>(qx[c], qrow + d0);
-          raw_load8<T>(qy[c], qrow + d0 + HALF);
-          load_cs8(cs + d0, qc[c], qs[c]);
-        } else {
-          qx[c][0] = __float_as_uint(to_f(qrow[d0]));
-          qy[c][0] = __float_as_uint(to_f(qrow[d0 + HALF]));
-          const float2 w = cs[d0];
-          qc[c][0] = w.x;
-          qs[c][0] = w.y;
-        }
+      if constexpr (KPL == 8) {
+        raw_load8<T>(qx[c], qrow + d0);
+        raw_load8<T>(qy[c], qrow + d0 + HALF);
+        load_cs8(cs + d0, qc[c], qs[c]);
+      } else {
+        qx[c][0] = __float_as_uint(to_f(qrow[d0]));
+        qy[c][0] = __float_as_uint(to_f(qrow[d0 + HALF]));
+        const float2 w = cs[d0];
+        qc[c][0] = w.x;
+        qs[c][0] = w.y;
       }
     }
-    if (t0 < nct) ld.template fetch_data<false>(t0);
-    else ld.template fetch_data<true>(tile_of(t0));
+    ld.template fetch_data<SUF>(SUF ? tile_of(t0) : t0);
 #pragma unroll
     for (int c = 0; c < NQC / 2; ++c) {
       float x[KPL], y[KPL];
-      if (row_ok) {
-        if constexpr (KPL == 8) {
-          raw_to_f8<T>(qx[c], x);
-          raw_to_f8<T>(qy[c], y);
-        } else {
-          x[0] = __uint_as_float(qx[c][0]);
-          y[0] = __uint_as_float(qy[c][0]);
-        }
-#pragma unroll
-        for (int e = 0; e < KPL; ++e) {
-          rotate_pair(x[e], y[e], qc[c][e], qs[c][e]);
-          x[e] *= a.qscale;
-          y[e] *= a.qscale;
-        }
+      if constexpr (KPL == 8) {
+        raw_to_f8<T>(qx[c], x);
+        raw_to_f8<T>(qy[c], y);
       } else {
+        x[0] = __uint_as_float(qx[c][0]);
+        y[0] = __uint_as_float(qy[c][0]);
+      }
 #pragma unroll
-        for (int e = 0; e < KPL; ++e) { x[e] = 0.f; y[e] = 0.f; }
+      for (int e = 0; e < KPL; ++e) {
+        rotate_pair(x[e], y[e], qc[c][e], qs[c][e]);
+        x[e] *= a.qscale;
+        y[e] *= a.qscale;
       }
       if constexpr (KPL == 1) {
         qop[c] = x[0];
@@ -854,7 +852,9 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         }
       }
     }
-  }
+  };
+  if (t0 < nct) q_prologue(std::false_type{});
+  else q_prologue(std::true_type{});
 
   float m_run = kNegInf, l_run = 0.f;
   f32x16 o[NDB];
