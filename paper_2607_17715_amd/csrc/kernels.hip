@@ -300,6 +300,10 @@ struct Shape {
   static constexpr int VU_TOT = (KT / 2) * (D / 8);// value units: 8-element chunk of 2 keys
   static constexpr int NKU = (KU_TOT + NT - 1) / NT;
   static constexpr int NVU = (VU_TOT + NT - 1) / NT;
+  // every thread's units all inside the tile: no per-unit guard (a guarded
+  // load leaves the compiler's wait counts conservative after it)
+  static constexpr bool KU_ALL = KU_TOT % NT == 0;
+  static constexpr bool VU_ALL = VU_TOT % NT == 0;
   static constexpr int EPV = 16 / sizeof(T);       // elements per 16-byte vector
   static constexpr int PK_TOT = KT * D / EPV;      // page vectors, keys
   static constexpr int PV_TOT = D * KT / EPV;      // page vectors, transposed values
@@ -568,7 +572,7 @@ struct TileLoader {
         const int kk = u / KUPK, c = u % KUPK;
         uint32_t* w = rk + i * 2 * Sh::WA;
         k_ok[i] = u < Sh::KU_TOT && kk < nvalid;
-        if (u < Sh::KU_TOT) {                 // uniform per wavefront
+        if (Sh::KU_ALL || u < Sh::KU_TOT) {   // uniform per wavefront
           const size_t tok = size_t(b) * S + k0 + min(kk, nvalid - 1);
           const size_t row = tok * a.Hkv + g;
           raw_load8<T>(w, ksuf + row * D + 8 * c);
@@ -585,7 +589,7 @@ struct TileLoader {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           v_ok[j] = u < Sh::VU_TOT && kp2 + j < nvalid;
-          if (u < Sh::VU_TOT) {
+          if (Sh::VU_ALL || u < Sh::VU_TOT) {
             const size_t row = (size_t(b) * S + k0 + min(kp2 + j, nvalid - 1)) * a.Hkv + g;
             raw_load8<T>(w + j * Sh::WA, vsuf + row * D + 8 * c);
           }
@@ -594,23 +598,10 @@ struct TileLoader {
     } else if constexpr (kPaged) {
       paged_fetch(k0, rk, rv);
     } else {
-#pragma unroll
-      for (int i = 0; i < Sh::NKU; ++i) {
-        const int u = tid + i * NT;
-        const int c = u % KUPK;
-        uint32_t* w = rk + i * 2 * Sh::WP;
-        k_ok[i] = nk_ok[i];
-        if (u < Sh::KU_TOT) {
-          const size_t row = size_t(nk[i].x) * a.Hkv + g;
-          raw_load8<PoolT>(w, kpool + row * D + 8 * c);
-          raw_load8<PoolT>(w + Sh::WP, kpool + row * D + 8 * c + HALF);
-          if constexpr (SRC == SRC_POOL_I8) k_scale[i] = a.k_scale[row];
-          if (nk[i].y != cs_seg[i]) {       // a segment's cos/sin stay until it changes
-            load_cs8(a.seg_cs + size_t(nk[i].y) * HALF + 8 * c, ck[i], sk[i]);
-            cs_seg[i] = nk[i].y;
-          }
-        }
-      }
+      // values, then keys, then the keys' cos/sin, which are loaded only where a
+      // key unit's segment changes: the compiler's count of the loads in flight
+      // is exact up to such a load and conservative after it, so the rows it
+      // follows are not made to wait for each other
 #pragma unroll
       for (int i = 0; i < Sh::NVU; ++i) {
         const int u = tid + i * NT;
@@ -619,11 +610,33 @@ struct TileLoader {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           v_ok[j] = u < Sh::VU_TOT && nv_ok[j];
-          if (u < Sh::VU_TOT) {
+          if (Sh::VU_ALL || u < Sh::VU_TOT) {
             const size_t row = size_t(nv[j]) * a.Hkv + g;
             raw_load8<PoolT>(w + j * Sh::WP, vpool + row * D + 8 * c);
             if constexpr (SRC == SRC_POOL_I8) v_scale[j] = a.v_scale[row];
           }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < Sh::NKU; ++i) {
+        const int u = tid + i * NT;
+        const int c = u % KUPK;
+        uint32_t* w = rk + i * 2 * Sh::WP;
+        k_ok[i] = nk_ok[i];
+        if (Sh::KU_ALL || u < Sh::KU_TOT) {
+          const size_t row = size_t(nk[i].x) * a.Hkv + g;
+          raw_load8<PoolT>(w, kpool + row * D + 8 * c);
+          raw_load8<PoolT>(w + Sh::WP, kpool + row * D + 8 * c + HALF);
+          if constexpr (SRC == SRC_POOL_I8) k_scale[i] = a.k_scale[row];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < Sh::NKU; ++i) {
+        const int u = tid + i * NT;
+        const int c = u % KUPK;
+        if ((Sh::KU_ALL || u < Sh::KU_TOT) && nk[i].y != cs_seg[i]) {   // a segment's cos/sin stay until it changes
+          load_cs8(a.seg_cs + size_t(nk[i].y) * HALF + 8 * c, ck[i], sk[i]);
+          cs_seg[i] = nk[i].y;
         }
       }
     }
@@ -638,7 +651,7 @@ struct TileLoader {
 #pragma unroll
       for (int i = 0; i < Sh::NKU; ++i) {
         const int u = tid + i * NT;
-        if (u >= Sh::KU_TOT) continue;
+        if (!Sh::KU_ALL && u >= Sh::KU_TOT) continue;
         const int kk = u / KUPK, c = u % KUPK;
         T* dst = sK + kk * L::LDK + 8 * c;
         if (nvalid < KT && !k_ok[i]) {        // only a partial tile has such keys
@@ -669,7 +682,7 @@ struct TileLoader {
 #pragma unroll
       for (int i = 0; i < Sh::NVU; ++i) {
         const int u = tid + i * NT;
-        if (u >= Sh::VU_TOT) continue;
+        if (!Sh::VU_ALL && u >= Sh::VU_TOT) continue;
         const int c = u / (KT / 2);
         // bf16 values that need no decode: a transposed word holds element e of
         // the two keys kp2 and kp2 + 1, i.e. one 16-bit half of each row's word
