@@ -1271,6 +1271,27 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
   float li[NPS];
 #pragma unroll
   for (int k = 0; k < NPS; ++k) li[k] = pl[size_t(min(sub + k * TPR, last)) * a.RB];
+  // the first 16 splits' partial rows load together with the LSEs (their
+  // addresses do not depend on them): one memory round trip instead of two
+  const T* po = static_cast<const T*>(a.part_o) + (size_t(mg.part0) * a.RB + rloc) * D + sub * EPT;
+  float v[16][EPT];
+  auto load_batch = [&](int i0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const T* src = po + size_t(min(i0 + k, last)) * a.RB * D;
+      if constexpr (sizeof(T) == 4) {
+        const float4 x = *reinterpret_cast<const float4*>(src);
+        v[k][0] = x.x; v[k][1] = x.y; v[k][2] = x.z; v[k][3] = x.w;
+      } else {
+        const uint2 u = *reinterpret_cast<const uint2*>(src);
+        v[k][0] = __uint_as_float(u.x << 16);
+        v[k][1] = __uint_as_float(u.x & 0xffff0000u);
+        v[k][2] = __uint_as_float(u.y << 16);
+        v[k][3] = __uint_as_float(u.y & 0xffff0000u);
+      }
+    }
+  };
+  load_batch(0);
   float mx = kNegInf;
 #pragma unroll
   for (int k = 0; k < NPS; ++k) {
@@ -1292,25 +1313,8 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
   __syncthreads();
 
   float acc[EPT] = {};
-  const T* po = static_cast<const T*>(a.part_o) + (size_t(mg.part0) * a.RB + rloc) * D + sub * EPT;
   for (int i0 = 0; i0 < mg.nsplit; i0 += 16) {
-    float v[16][EPT];
-#pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      {
-        const T* src = po + size_t(min(i0 + k, last)) * a.RB * D;
-        if constexpr (sizeof(T) == 4) {
-          const float4 x = *reinterpret_cast<const float4*>(src);
-          v[k][0] = x.x; v[k][1] = x.y; v[k][2] = x.z; v[k][3] = x.w;
-        } else {
-          const uint2 u = *reinterpret_cast<const uint2*>(src);
-          v[k][0] = __uint_as_float(u.x << 16);
-          v[k][1] = __uint_as_float(u.x & 0xffff0000u);
-          v[k][2] = __uint_as_float(u.y << 16);
-          v[k][3] = __uint_as_float(u.y & 0xffff0000u);
-        }
-      }
-    }
+    if (i0 > 0) load_batch(i0);
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
       const int i = i0 + k;
