@@ -29,6 +29,9 @@ import time
 
 import numpy as np
 
+sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+import synth  # noqa: E402  (seeded input generators; shapes of the workloads)
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -56,13 +59,15 @@ WORKLOADS = {
     "int8-layer-host-load": 4,
     "sif-extract-llama3-8b-bf16": 0,
 }
+# decode steps over the rest of the context x compression grid (Section 4.3)
+for _i, (_ctx, _r) in enumerate(synth.DECODE_GRID):
+    WORKLOADS[f"decode-{_ctx}k-{_r}x-bf16"] = 12 + _i
 # extraction-time attention with Structured Information Flow over document chunks
 SIF = {"sif-extract-llama3-8b-bf16"}
 DEFAULT_WORKLOAD = "llama3-8b-layer-bf16"
 LONG_SUFFIX = {"70b-long-suffix-bf16"}
 # one generated token over a cache composed once beforehand: the step is c2kv_attend
-DECODE = {"decode-32k-4x-bf16", "decode-128k-4x-bf16", "decode-128k-16x-bf16",
-          "decode-128k-1x-bf16"}
+DECODE = {name for name, idx in WORKLOADS.items() if 6 <= idx <= 9 or idx >= 12}
 # the load step: chunks stored compressed in page-locked host memory, read in place by the
 # fused kernel over the host link, or copied to the device first (c2kv_load)
 HOST_ZEROCOPY = {"llama3-8b-layer-host-zerocopy", "int8-layer-host-zerocopy"}
@@ -329,7 +334,6 @@ def main():
 
     import torch
     import paper_2607_17715_amd as c2kv
-    import synth
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib << 20

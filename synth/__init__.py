@@ -190,7 +190,18 @@ def spec(idx: int) -> Spec:
     if idx == 11:
         return Spec("llama3-8b-layer-c2x4-bf16", 32, 8, 128, 5e5, "bf16", "bf16", 8, 512, 64,
                     1, 8, "shuffled", ("c2", 4), 64)
+    # the rest of the decode grid: contexts of 16k-128k tokens, uncompressed or
+    # with 4x / 8x / 16x compression (Section 4.3)
+    if 12 <= idx < 12 + len(DECODE_GRID):
+        ctx, r = DECODE_GRID[idx - 12]
+        return Spec(f"decode-{ctx}k-{r}x-bf16", 32, 8, 128, 5e5, "bf16", "bf16", ctx // 2, 2048,
+                    0, 1, ctx // 2, "natural", ("all",) if r == 1 else ("count", 2048 // r), 1)
     raise ValueError(idx)
+
+
+# (context in thousands of tokens, compression) of decode workloads 12 and on
+DECODE_GRID = [(16, 1), (16, 4), (16, 8), (16, 16), (32, 1), (32, 8), (32, 16),
+               (64, 1), (64, 4), (64, 8), (64, 16), (128, 8)]
 
 
 def _kept_for_chunk(rng: np.random.Generator, keep: tuple, n: int) -> np.ndarray:

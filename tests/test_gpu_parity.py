@@ -77,6 +77,12 @@ def test_decode_128k_4x():
     _both_paths(synth.config(7), "decode-128k-4x")
 
 
+@pytest.mark.parametrize("idx", [12, 14, 15])
+def test_decode_16k_grid(idx):
+    """The 16k-context decode, uncompressed and at 8x and 16x, at full size."""
+    _both_paths(synth.config(idx), synth.spec(idx).name)
+
+
 @pytest.mark.parametrize("suffix_len", [1, 7, 25])
 @pytest.mark.parametrize("opts", [dict(kv_splits=1), dict(kv_splits=2), dict(kv_splits=3),
                                   dict(kv_splits=5), dict(kv_splits=3, page_size=128)])

@@ -44,7 +44,7 @@ def _assert_layout_equal(w, plan):
     np.testing.assert_array_equal(dl, np.concatenate(lay["delta"]) if len(dl) else dl)
 
 
-@pytest.mark.parametrize("idx", [1, 2, 4, 5, 6, 10, 11])
+@pytest.mark.parametrize("idx", [1, 2, 4, 5, 6, 10, 11, 13, 18])
 def test_layout_bit_exact_configs(idx):
     w = synth.config(idx)
     _assert_layout_equal(w, c2kv.Plan.for_workload(w))
