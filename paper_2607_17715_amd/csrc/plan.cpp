@@ -345,8 +345,10 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       }
     }
   }
-  // the in-kernel merge serialises a row block's combine in one workgroup,
-  // which measured slower than the separate merge kernel at every split count
+  // never chosen automatically: each split's agent-scope release writes back its
+  // XCD's whole L2 and the last split's acquire invalidates it, which costs the
+  // other workgroups there their cached keys and values (measured 2-5x slower
+  // than the separate merge kernel)
   p.merge_in_kernel = o.merge_mode == 1;
 
   // XCD-aware order.  Workgroups are dealt to the 8 XCDs round-robin by index,
