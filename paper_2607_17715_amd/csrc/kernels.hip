@@ -926,16 +926,39 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
     const bool suffix = tile >= nct;
     const int k0 = suffix ? (tile - nct) * KT : tile * KT;
     const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
-    if (suffix || nvalid < KT) {
-      const RowKeys row_keys(t, a);        // SIF kernels only (unused otherwise)
+    if constexpr (kSif) {
+      if (suffix || nvalid < KT) {
+        const RowKeys row_keys(t, a);
+#pragma unroll
+        for (int j = 0; j < NKB; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int key = (kh * NKB + j) * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+            const int u = k0 + key;
+            const bool vis = key < nvalid && (!suffix || row_keys.sees(u));
+            if (!vis) s[j][v] = kNegInf;
+          }
+      }
+    } else if (suffix || nvalid < KT) {
+      // key = base + off with off a constant per accumulator value, visible
+      // where off <= lim.  In a suffix tile u <= t < S already implies
+      // key < nvalid; a cached tile has no causal part.  A masked score's bits
+      // are replaced by -inf's through the sign of lim - off (v_bfi_b32): no
+      // compares, whose 64-bit lane masks the compiler kept live all at once,
+      // spilling scalar registers into the key loop
+      const int base = kh * NKB * 32 + 4 * half;
+      const int lim = suffix ? t - k0 - base : nvalid - 1 - base;
 #pragma unroll
       for (int j = 0; j < NKB; ++j)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int key = (kh * NKB + j) * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-          const int u = k0 + key;
-          const bool vis = key < nvalid && (!suffix || (kSif ? row_keys.sees(u) : u <= t));
-          if (!vis) s[j][v] = kNegInf;
+          const int off = j * 32 + 8 * (v >> 2) + (v & 3);
+          uint32_t x = __float_as_uint(s[j][v]), m;
+          asm("v_subrev_u32 %1, %3, %2\n\t"       // lim - off
+              "v_ashrrev_i32 %1, 31, %1\n\t"      // all ones where masked
+              "v_bfi_b32 %0, %1, %4, %0"
+              : "+v"(x), "=&v"(m) : "v"(lim), "i"(off), "v"(0xff800000u));
+          s[j][v] = __uint_as_float(x);
         }
     }
     float mt = kNegInf;
