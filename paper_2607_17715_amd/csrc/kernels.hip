@@ -1459,10 +1459,23 @@ __global__ __launch_bounds__(256) void merge_split_kernel(MergeParams a) {
 // compose: gather -> decode -> turn -> paged write
 // ----------------------------------------------------------------------------
 
+// One workgroup per (key tile, kv-head).  Three phases, so that every load of
+// a thread is in flight at once: the slot indices of its key and value units,
+// then all rows and cos/sin, then the turned keys and the transposed values
+// (through LDS) are written.  Loads are unconditional (indices clamped into the
+// tile); keys and values past the tile's end are written as zeros.
 template <typename T, int D, typename PoolT>
 __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
   using L = Lds<T, D>;
+  constexpr int NTH = 256;
+  constexpr int KU = D / 16;                 // key units per key: 8-element pairs (c, c + D/2)
+  constexpr int NKU = KT * KU / NTH;         // key units per thread
+  constexpr int VU = D / 8;                  // value units per key: 8 elements
+  constexpr int NVU = KT * VU / NTH;         // value units per thread (one key: tid % KT)
+  static_assert(KT * KU % NTH == 0 && KT * VU % NTH == 0 && NTH % KT == 0,
+                "every thread holds whole units of one value key");
   __shared__ __attribute__((aligned(16))) T sV[D * L::LDV];
+  const int tid = threadIdx.x;
   const int b = a.tiles[2 * blockIdx.x], tile = a.tiles[2 * blockIdx.x + 1];
   const int g = blockIdx.y;
   const int slot0 = a.req_slot0[b];
@@ -1477,60 +1490,74 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
   const PoolT* kpool = static_cast<const PoolT*>(a.k);
   const PoolT* vpool = static_cast<const PoolT*>(a.v);
 
-  // keys: straight to the page, turned by delta
-  constexpr int KU = D / 16;
-  for (int u = threadIdx.x; u < KT * KU; u += blockDim.x) {
-    const int kk = u / KU, c = u % KU;
-    T* dst = kpage + size_t(kk) * D + 8 * c;
-    if (kk < nvalid) {
-      const int slot = slot0 + k0 + kk;
-      const int2 si = a.slot_info[slot];
-      const size_t row = size_t(si.x) * a.Hkv + g;
-      float x[8], y[8], cc[8], ss[8];
-      load8(kpool + row * D + 8 * c, x);
-      load8(kpool + row * D + 8 * c + D / 2, y);
-      if constexpr (sizeof(PoolT) == 1) {
-        const float ks = a.k_scale[row];
+  // ---- slot indices
+  int2 ks[NKU];
+  int kpos[NKU];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) { x[e] *= ks; y[e] *= ks; }
-      }
-      load_cs8(a.seg_cs + size_t(si.y) * (D / 2) + 8 * c, cc, ss);
-      rotate8(x, y, cc, ss);
-      store8(dst, x);
-      store8(dst + D / 2, y);
-      if (g == 0 && c == 0) {
-        if (a.out_src_row) a.out_src_row[slot] = si.x;
-        if (a.out_pos) a.out_pos[slot] = a.slot_pos[slot];
-      }
-    } else {
-      store8_zero(dst);
-      store8_zero(dst + D / 2);
+  for (int i = 0; i < NKU; ++i) {
+    const int slot = slot0 + k0 + min((tid + i * NTH) / KU, nvalid - 1);
+    ks[i] = a.slot_info[slot];
+    kpos[i] = a.out_pos ? a.slot_pos[slot] : 0;
+  }
+  const int vkk = tid % KT;
+  const int vsrc = a.slot_info[slot0 + k0 + min(vkk, nvalid - 1)].x;
+
+  // ---- rows, scales and cos/sin
+  float kx[NKU][8], ky[NKU][8], kc[NKU][8], kn[NKU][8], vx[NVU][8];
+  float kscale[NKU], vscale = 1.f;
+  const size_t vrow = size_t(vsrc) * a.Hkv + g;
+#pragma unroll
+  for (int i = 0; i < NVU; ++i) load8(vpool + vrow * D + 8 * ((tid + i * NTH) / KT), vx[i]);
+  if constexpr (sizeof(PoolT) == 1) vscale = a.v_scale[vrow];
+#pragma unroll
+  for (int i = 0; i < NKU; ++i) {
+    const int c = (tid + i * NTH) % KU;
+    const size_t row = size_t(ks[i].x) * a.Hkv + g;
+    load8(kpool + row * D + 8 * c, kx[i]);
+    load8(kpool + row * D + 8 * c + D / 2, ky[i]);
+    kscale[i] = 1.f;
+    if constexpr (sizeof(PoolT) == 1) kscale[i] = a.k_scale[row];
+    load_cs8(a.seg_cs + size_t(ks[i].y) * (D / 2) + 8 * c, kc[i], kn[i]);
+  }
+
+  // (a scheduling fence: left to itself the scheduler waits for the first
+  // unit's rows before issuing the rest, to save registers)
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- keys: decoded, turned by delta, straight to the page.  Every unit is
+  // computed, past the tile's end with a zero scale: a branch there would sink
+  // loads into it, behind the others.
+#pragma unroll
+  for (int i = 0; i < NKU; ++i) {
+    const int u = tid + i * NTH;
+    const int kk = u / KU, c = u % KU;
+    const bool ok = kk < nvalid;
+    const float sc = ok ? kscale[i] : 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { kx[i][e] *= sc; ky[i][e] *= sc; }
+    rotate8(kx[i], ky[i], kc[i], kn[i]);
+    T* dst = kpage + size_t(kk) * D + 8 * c;
+    store8(dst, kx[i]);
+    store8(dst + D / 2, ky[i]);
+    if (ok && g == 0 && c == 0) {
+      const int slot = slot0 + k0 + kk;
+      if (a.out_src_row) a.out_src_row[slot] = ks[i].x;
+      if (a.out_pos) a.out_pos[slot] = kpos[i];
     }
   }
-  // values: transpose through LDS, then write each d-row of the page segment
-  constexpr int VU = D / 8;
-  for (int u = threadIdx.x; u < KT * VU; u += blockDim.x) {
-    const int c = u / KT, kk = u % KT;
-    float x[8];
-    if (kk < nvalid) {
-      const size_t row = size_t(a.slot_info[slot0 + k0 + kk].x) * a.Hkv + g;
-      load8(vpool + row * D + 8 * c, x);
-      if constexpr (sizeof(PoolT) == 1) {
-        const float vs = a.v_scale[row];
+  // ---- values: decoded, transposed through LDS, then each d-row of the page segment
+  const bool vok = vkk < nvalid;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] *= vs;
-      }
-    } else {
+  for (int i = 0; i < NVU; ++i) {
+    const int c = (tid + i * NTH) / KT;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = 0.f;
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) sV[(8 * c + e) * L::LDV + kk] = from_f<T>(x[e]);
+    for (int e = 0; e < 8; ++e)
+      sV[(8 * c + e) * L::LDV + vkk] = from_f<T>(vok ? vx[i][e] * vscale : 0.f);
   }
   __syncthreads();
   constexpr int EPV = 16 / sizeof(T);
   constexpr int VV = KT / EPV;
-  for (int u = threadIdx.x; u < D * VV; u += blockDim.x) {
+  for (int u = tid; u < D * VV; u += NTH) {
     const int d = u / VV, vec = u % VV;
     const uint2* src = reinterpret_cast<const uint2*>(sV + d * L::LDV + vec * EPV);
     const uint2 lo = src[0], hi = src[1];     // LDS rows are 8-byte aligned
