@@ -255,13 +255,11 @@ struct AttnParams {
 };
 
 struct ComposeParams {
-  int Hkv, PS, max_pages;
-  const int* req_slot0;
+  int Hkv, PS;
   const int2* slot_info;
   const int* slot_pos;
   const float2* seg_cs;
-  const int* block_table;
-  const int* tiles;            // [n][2] (b, tile)
+  const int4* tiles;           // [n] (first slot, keys in the tile, page, offset in it)
   const void* k;               // pool
   const void* v;
   const float* k_scale;
@@ -1476,15 +1474,10 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
                 "every thread holds whole units of one value key");
   __shared__ __attribute__((aligned(16))) T sV[D * L::LDV];
   const int tid = threadIdx.x;
-  const int b = a.tiles[2 * blockIdx.x], tile = a.tiles[2 * blockIdx.x + 1];
+  const int4 tl = a.tiles[blockIdx.x];
   const int g = blockIdx.y;
-  const int slot0 = a.req_slot0[b];
-  const int N = a.req_slot0[b + 1] - slot0;
-  const int k0 = tile * KT;
-  const int nvalid = min(KT, N - k0);
-  const int page = a.block_table[size_t(b) * a.max_pages + k0 / a.PS];
-  const int off = k0 % a.PS;
-  const size_t ph = size_t(page) * a.Hkv + g;
+  const int first = tl.x, nvalid = tl.y, off = tl.w;   // slots [first, first + nvalid)
+  const size_t ph = size_t(tl.z) * a.Hkv + g;
   T* kpage = static_cast<T*>(a.k_pages) + (ph * a.PS + off) * D;
   T* vpage = static_cast<T*>(a.v_pages) + ph * D * a.PS + off;
   const PoolT* kpool = static_cast<const PoolT*>(a.k);
@@ -1495,12 +1488,12 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
   int kpos[NKU];
 #pragma unroll
   for (int i = 0; i < NKU; ++i) {
-    const int slot = slot0 + k0 + min((tid + i * NTH) / KU, nvalid - 1);
+    const int slot = first + min((tid + i * NTH) / KU, nvalid - 1);
     ks[i] = a.slot_info[slot];
     kpos[i] = a.out_pos ? a.slot_pos[slot] : 0;
   }
   const int vkk = tid % KT;
-  const int vsrc = a.slot_info[slot0 + k0 + min(vkk, nvalid - 1)].x;
+  const int vsrc = a.slot_info[first + min(vkk, nvalid - 1)].x;
 
   // ---- rows, scales and cos/sin
   float kx[NKU][8], ky[NKU][8], kc[NKU][8], kn[NKU][8], vx[NVU][8];
@@ -1540,7 +1533,7 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
     store8(dst, kx[i]);
     store8(dst + D / 2, ky[i]);
     if (ok && g == 0 && c == 0) {
-      const int slot = slot0 + k0 + kk;
+      const int slot = first + kk;
       if (a.out_src_row) a.out_src_row[slot] = ks[i].x;
       if (a.out_pos) a.out_pos[slot] = kpos[i];
     }
@@ -1711,18 +1704,15 @@ hipError_t launch_compose(const Plan& p, int pool_dtype, const void* k, const vo
                           const float* k_scale, const float* v_scale, void* k_pages,
                           void* v_pages, int64_t* out_src_row, int32_t* out_pos,
                           hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-  const int n_tiles = static_cast<int>(p.compose_tiles.size() / 2);
+  const int n_tiles = static_cast<int>(p.compose_tiles.size() / 4);
   if (n_tiles == 0) return hipSuccess;
   ComposeParams cp{};
   cp.Hkv = p.cfg.n_kv_heads;
   cp.PS = p.page_size;
-  cp.max_pages = p.max_pages;
-  cp.req_slot0 = at<int>(p.d_workspace, p.ws.req_slot0);
   cp.slot_info = at<int2>(p.d_workspace, p.ws.slot_info);
   cp.slot_pos = at<int>(p.d_workspace, p.ws.slot_pos);
   cp.seg_cs = at<float2>(p.d_workspace, p.ws.seg_cs);
-  cp.block_table = at<int>(p.d_workspace, p.ws.block_table);
-  cp.tiles = at<int>(p.d_workspace, p.ws.compose_tiles);
+  cp.tiles = at<int4>(p.d_workspace, p.ws.compose_tiles);
   cp.k = k;
   cp.v = v;
   cp.k_scale = k_scale;

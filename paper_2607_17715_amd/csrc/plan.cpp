@@ -234,11 +234,16 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   }
   if (pages > kI32Max) { err = "too many pages"; return C2KV_E_UNSUPPORTED; }
   p.n_pages = static_cast<int32_t>(pages);
+  // compose tiles carry what their workgroup needs, so that it starts with one
+  // scalar load: first slot, keys in the tile, page and offset in the page
   for (int b = 0; b < B; ++b) {
     const int64_t n = p.req_slot0[b + 1] - p.req_slot0[b];
     for (int t = 0; t < ceil_div(n, kKeyTile); ++t) {
-      p.compose_tiles.push_back(b);
-      p.compose_tiles.push_back(t);
+      const int64_t k0 = int64_t(t) * kKeyTile;
+      p.compose_tiles.push_back(static_cast<int32_t>(p.req_slot0[b] + k0));
+      p.compose_tiles.push_back(static_cast<int32_t>(std::min<int64_t>(kKeyTile, n - k0)));
+      p.compose_tiles.push_back(p.block_table[size_t(b) * maxp + k0 / PS]);
+      p.compose_tiles.push_back(static_cast<int32_t>(k0 % PS));
     }
   }
 

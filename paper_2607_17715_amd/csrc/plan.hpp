@@ -44,7 +44,7 @@ struct WorkspaceLayout {
   size_t seg_cs = 0;      // float2 [n_seg][D/2]   cos/sin(delta * theta_i)
   size_t suf_cs = 0;      // float2 [B][S][D/2]    cos/sin((span_end + t) * theta_i)
   size_t block_table = 0; // int32 [B][max_pages]
-  size_t compose_tiles = 0; // int32x2 [n_compose_tiles] (b, tile)
+  size_t compose_tiles = 0; // int32x4 [n_compose_tiles] (first slot, keys, page, offset)
   size_t items = 0;       // WorkItem [n_items]
   size_t merges = 0;      // MergeGroup [n_merge]
   size_t counters = 0;    // int32 [n_merge], zero between launches
@@ -78,7 +78,7 @@ struct Plan {
   // pages
   int32_t n_pages = 0, max_pages = 0;
   std::vector<int32_t> block_table;   // [B][max_pages]
-  std::vector<int32_t> compose_tiles; // [n][2]
+  std::vector<int32_t> compose_tiles; // [n][4]
 
   // attention work decomposition
   int32_t rows_per_block = 128;
