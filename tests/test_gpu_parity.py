@@ -240,6 +240,17 @@ def test_empty_and_long_requests_in_one_batch():
     _both_paths(w, "empty request in batch")
 
 
+@pytest.mark.parametrize("heads", [(4, 4), (8, 4), (12, 4), (32, 2)])
+@pytest.mark.parametrize("rows_per_block", [64, 128, 256])
+def test_gqa_group_sizes(heads, rows_per_block):
+    """Query heads per kv-head G = 1, 2, 3 and 16: a row block's rows r = t*G + (h mod G)
+    then start and end at any head of a token."""
+    hq, hkv = heads
+    w = synth.small(batch=2, n_q_heads=hq, n_kv_heads=hkv, suffix_len=37,
+                    keep=("ratio", 0.2, 0.8), seed=40 + hq)
+    _both_paths(w, f"G={hq // hkv} rows={rows_per_block}", rows_per_block=rows_per_block)
+
+
 def test_head_dim_64_bf16_and_int8():
     for dt in ("bf16", "i8"):
         _both_paths(synth.small(pool_dtype=dt, head_dim=64, batch=2), f"d=64 {dt}")
