@@ -455,6 +455,22 @@ def main():
     roof["kernel_avg_us"] = kern[dom]["avg_us"]
     roof["algorithmic_bytes"] = dom_bytes
     roof["algorithmic_flops"] = work["flops"]
+    compose_roof = None
+    if "compose" in kern:
+        # the gather / dequant / re-rotation / page write step on its own: kept rows read
+        # in the storage dtype (and their scales), composed rows written in the
+        # activation dtype
+        b_pool = {"f32": 4, "bf16": 2, "i8": 1}[w.pool_dtype]
+        b_act = {"f32": 4, "bf16": 2}[w.act_dtype]
+        n_tok = int(composed.sum())
+        c_bytes = n_tok * w.n_kv_heads * (2 * w.head_dim * (b_pool + b_act)
+                                          + (8 if w.pool_dtype == "i8" else 0))
+        c_s = kern["compose"]["avg_us"] * 1e-6
+        compose_roof = {"bound": "hbm", "achieved": c_bytes / c_s / 1e9, "peak": PEAK_HBM_GBS,
+                        "unit": "GB/s", "frac": c_bytes / c_s / 1e9 / PEAK_HBM_GBS,
+                        "traffic": load_traffic(args.workload, "compose", c_bytes),
+                        "kernel": "compose", "kernel_avg_us": kern["compose"]["avg_us"],
+                        "algorithmic_bytes": c_bytes}
 
     result = {
         "metric": METRIC,
@@ -480,6 +496,7 @@ def main():
                             "merge_mode": args.merge_mode},
                    "input_copies": copies, "graph": graph_used},
         "roofline": roof,
+        **({"compose_roofline": compose_roof} if compose_roof else {}),
         "kernels_us": kern,
         "eager_ms_per_step": eager_ms,
         "source_sha": kernel_source_sha(),
