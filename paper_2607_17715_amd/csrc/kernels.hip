@@ -925,8 +925,14 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
     const int k0 = suffix ? (tile - nct) * KT : tile * KT;
     const int nvalid = suffix ? min(KT, S - k0) : min(KT, N - k0);
     if constexpr (kSif) {
-      if (suffix || nvalid < KT) {
-        const RowKeys row_keys(t, a);
+      const RowKeys row_keys(t, a);
+      // this wavefront's keys [w0, w1] lie in one of the row's visible ranges for
+      // every lane (tiles below the causal diagonal): nothing to mask
+      const int w0 = k0 + kh * NKB * 32, w1 = w0 + NKB * 32 - 1;
+      const bool whole = nvalid == KT &&
+                         ((w0 >= row_keys.lo && w1 <= row_keys.hi) || w1 < row_keys.sink ||
+                          (w0 >= row_keys.blo && w1 < row_keys.bhi));
+      if (!__all(whole)) {
 #pragma unroll
         for (int j = 0; j < NKB; ++j)
 #pragma unroll
