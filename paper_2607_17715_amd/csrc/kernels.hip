@@ -920,6 +920,14 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 
   // ---- causal / ragged-tail mask, then the new running maximum (base 2);
   // accumulator value v of block kb holds key 32*kb + 8*(v/4) + 4*half + v%4
+  auto max_of = [](const f32x16 (&s)[NKB]) {
+    float mt = kNegInf;
+#pragma unroll
+    for (int j = 0; j < NKB; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s[j][v]);
+    return mt;
+  };
   auto mask_max = [&](int tile, f32x16 (&s)[NKB]) {
     const bool suffix = tile >= nct;
     const int k0 = suffix ? (tile - nct) * KT : tile * KT;
@@ -952,25 +960,23 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
       // spilling scalar registers into the key loop
       const int base = kh * NKB * 32 + 4 * half;
       const int lim = suffix ? t - k0 - base : nvalid - 1 - base;
+      // (suffix tiles below the diagonal: every lane sees all its keys)
+      if (!__all(lim >= 32 * (NKB - 1) + 27)) {
 #pragma unroll
-      for (int j = 0; j < NKB; ++j)
+        for (int j = 0; j < NKB; ++j)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int off = j * 32 + 8 * (v >> 2) + (v & 3);
-          uint32_t x = __float_as_uint(s[j][v]), m;
-          asm("v_subrev_u32 %1, %3, %2\n\t"       // lim - off
-              "v_ashrrev_i32 %1, 31, %1\n\t"      // all ones where masked
-              "v_bfi_b32 %0, %1, %4, %0"
-              : "+v"(x), "=&v"(m) : "v"(lim), "i"(off), "v"(0xff800000u));
-          s[j][v] = __uint_as_float(x);
-        }
+          for (int v = 0; v < 16; ++v) {
+            const int off = j * 32 + 8 * (v >> 2) + (v & 3);
+            uint32_t x = __float_as_uint(s[j][v]), m;
+            asm("v_subrev_u32 %1, %3, %2\n\t"       // lim - off
+                "v_ashrrev_i32 %1, 31, %1\n\t"      // all ones where masked
+                "v_bfi_b32 %0, %1, %4, %0"
+                : "+v"(x), "=&v"(m) : "v"(lim), "i"(off), "v"(0xff800000u));
+            s[j][v] = __uint_as_float(x);
+          }
+      }
     }
-    float mt = kNegInf;
-#pragma unroll
-    for (int j = 0; j < NKB; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s[j][v]);
-    return fmaxf(m_run, half_pair_max(mt));
+    return fmaxf(m_run, half_pair_max(max_of(s)));
   };
 
   // ---- rescale the running sum and output to a new maximum
