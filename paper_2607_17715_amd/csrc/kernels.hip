@@ -941,14 +941,33 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
                          ((w0 >= row_keys.lo && w1 <= row_keys.hi) || w1 < row_keys.sink ||
                           (w0 >= row_keys.blo && w1 < row_keys.bhi));
       if (!__all(whole)) {
+        // the lane's visible keys among the wavefront's [w0, w0 + 32 NKB) as a bit
+        // mask (bit k: key w0 + k), shifted so that accumulator value (j, v)
+        // tests bit 32 j + 8 (v / 4) + v % 4, a constant: one bit-field extract and
+        // one bit select per score
+        auto bits = [](int x0, int x1) -> uint64_t {   // keys [x0, x1) relative to w0
+          x0 = max(x0, 0);
+          x1 = min(x1, 64);
+          if (x1 <= x0) return 0;
+          const uint64_t below1 = x1 == 64 ? ~0ull : (1ull << x1) - 1;
+          return below1 & ~((1ull << x0) - 1);
+        };
+        uint64_t vis = bits(row_keys.lo - w0, row_keys.hi + 1 - w0) |
+                       bits(-w0, row_keys.sink - w0) |
+                       bits(row_keys.blo - w0, row_keys.bhi - w0);
+        vis &= bits(0, nvalid - kh * NKB * 32);
+        vis >>= 4 * half;
+        const uint32_t hidden[2] = {~uint32_t(vis), ~uint32_t(vis >> 32)};
 #pragma unroll
         for (int j = 0; j < NKB; ++j)
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const int key = (kh * NKB + j) * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-            const int u = k0 + key;
-            const bool vis = key < nvalid && (!suffix || row_keys.sees(u));
-            if (!vis) s[j][v] = kNegInf;
+            const int off = 8 * (v >> 2) + (v & 3);        // bit in word j
+            uint32_t x = __float_as_uint(s[j][v]), m;
+            asm("v_bfe_i32 %1, %2, %3, 1\n\t"          // all ones where hidden
+                "v_bfi_b32 %0, %1, %4, %0"
+                : "+v"(x), "=&v"(m) : "v"(hidden[j]), "i"(off), "v"(0xff800000u));
+            s[j][v] = __uint_as_float(x);
           }
       }
     } else if (suffix || nvalid < KT) {
