@@ -1279,7 +1279,11 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
     __threadfence();                       // release this split's partial (agent scope)
     __syncthreads();
     if (tid == 0) {
-      const int old = atomicAdd(a.counters + it.merge, 1);
+      // system scope: the splits of a row block may run on different XCDs, whose
+      // L2 caches are not coherent with each other; a system-scope atomic is
+      // performed past them
+      const int old = __hip_atomic_fetch_add(a.counters + it.merge, 1, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_SYSTEM);
       s_last = (old == a.merges[it.merge].nsplit - 1) ? 1 : 0;
     }
     __syncthreads();
@@ -1288,7 +1292,8 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
       const MergeGroup mg = a.merges[it.merge];
       merge_rows<T, D>(mg, 0, mg.nrows, a.part_o, a.part_lse, a.RB, a.Hq, G, S, a.out, a.lse,
                        tid, NT);
-      if (tid == 0) a.counters[it.merge] = 0;   // ready for the next launch
+      if (tid == 0)                        // ready for the next launch
+        __hip_atomic_store(a.counters + it.merge, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
   }
 }
