@@ -7,7 +7,9 @@
 //                    (Eq. 4): suffix RoPE on load, MFMA S^T = K Q^T, online
 //                    softmax in base 2, MFMA O^T = V^T P^T; keys come from the
 //                    pages, or straight from the pool (gather/decode/turn fused)
-//   merge_kernel     log-sum-exp combine of key splits
+//   merge_kernel     log-sum-exp combine of key splits, a thread per output
+//                    element; merge_split_kernel: one row per workgroup with
+//                    the splits spread over its lanes (many splits, few rows)
 //
 // MFMA use.  One wavefront owns 32 query rows.  Scores are computed transposed
 // (keys x queries) so that in the 32x32 accumulator layout every lane holds one
