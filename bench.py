@@ -110,11 +110,20 @@ def paged_attend_bytes(w, composed):
     return n_tok * (2 * Hkv * D * b_act + 4) + B * S * per_q
 
 
+def _code_only(text: str) -> str:
+    """C++ source without comments and blank space: what the compiler sees."""
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def kernel_source_sha() -> str:
+    """Hash of the code (comments and layout aside) of the kernels, the plan and the C ABI."""
     h = hashlib.sha256()
     for f in ("kernels.hip", "plan.cpp", "api.cpp"):
-        with open(os.path.join(ROOT, "paper_2607_17715_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2607_17715_amd", "csrc", f), encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
