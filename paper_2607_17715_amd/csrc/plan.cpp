@@ -251,7 +251,9 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
   const int64_t G = p.group, S = suffix_len;
   const int64_t R = G * S;            // query rows per (request, kv-head)
   int RB = o.rows_per_block;
-  if (RB == 0) RB = R >= 256 ? 256 : R > 64 ? 128 : 64;
+  // fp32 products (32x32x2 MFMA: eight times the instructions of bf16 per
+  // product) favour twice the workgroups of 64-row blocks below 256 rows
+  if (RB == 0) RB = R >= 256 ? 256 : R > 64 && cfg.act_dtype == C2KV_BF16 ? 128 : 64;
   p.rows_per_block = RB;
   // 8 wavefronts at 2 per SIMD fill a CU; 64-row blocks have 4 and run two to a CU
   const int wgs_per_cu = RB == 64 ? 2 : 1;
