@@ -808,9 +808,9 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   // ---- Q operand: RoPE at span_end + t, softmax scale and log2(e) folded in.
   // Lane (qi, half) holds d = c*KSTEP + half*KPL + e in qop[c][e]; the RoPE
   // partner d + D/2 sits in chunk c + NQC/2 of the same lane.
-  // The Q and cos/sin loads are issued first, then the first key tile's row
-  // loads (whose addresses wait only for the slot indices), and only then is Q
-  // rotated, so the two latencies overlap.  The two kinds of first tile take
+  // The first key tile's slot indices and the Q and cos/sin loads are issued
+  // first, then the tile's row loads (whose addresses wait only for the slot
+  // indices), and only then is Q rotated, so the two latencies overlap.  The two kinds of first tile take
   // copies of their own: where both kinds' loads could precede one wait, the
   // compiler counts the other kind's loads in flight too.
   Op qop[NQC];
