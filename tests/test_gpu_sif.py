@@ -77,3 +77,22 @@ def test_sif_original_rows_are_plain_causal_attention():
     out2, _, _ = _run(synth.dataclasses.replace(w, k=k2, v=v2))
     assert torch.equal(out[:, :n], out2[:, :n])
     assert not torch.equal(out[:, n:], out2[:, n:])
+
+
+@pytest.mark.parametrize("i", range(24))
+def test_sif_random_configurations(i):
+    """Seeded random SIF shapes: sequence length, block size (including blocks
+    longer than the sequence), sink, heads, head size, dtype and launch shape."""
+    r = np.random.default_rng(9100 + i)
+    n = int(r.integers(1, 400))
+    kw = dict(n_tokens=n, block=int(r.choice([1, 2, 3, 4, 8, 64, 500])),
+              sink=int(r.integers(0, min(n, 70) + 1)),
+              act_dtype=["bf16", "bf16", "f32"][r.integers(3)],
+              head_dim=int(r.choice([64, 128])))
+    hq, hkv = [(8, 2), (4, 4), (16, 4), (8, 1)][r.integers(4)]
+    opts = dict(rows_per_block=int(r.choice([0, 64, 128, 256])), kv_splits=int(r.choice([0, 0, 2])))
+    w = synth.sif(batch=int(r.integers(1, 3)), n_q_heads=hq, n_kv_heads=hkv, seed=9200 + i, **kw)
+    say(f"sif random {i}: {kw} H {hq}/{hkv} {opts}")
+    ref_out, ref_lse = _ref(w)
+    out, lse, _ = _run(w, **opts)
+    compare(w, out, lse, ref_out, ref_lse, what=f"sif random {i}")
