@@ -133,7 +133,10 @@ typedef struct c2kv_compose_desc {
 typedef struct c2kv_plan_opts {
   int32_t page_size;       /* tokens per page, a multiple of 64 (default 64)       */
   int32_t kv_splits;       /* > 0: key splits per row block (default: automatic)   */
-  int32_t rows_per_block;  /* 64, 128 or 256 query rows per workgroup (automatic) */
+  int32_t rows_per_block;  /* 64, 128 or 256 query rows per workgroup; automatic:
+                              256 when a (request, kv-head) has at least 256
+                              query rows (S * H_q / H_kv), else 128 (bf16, more
+                              than 64 rows) or 64                               */
   int32_t num_cus;         /* compute units to size the work list for (256)       */
   int32_t merge_mode;      /* combining key splits: 0 automatic (currently the
                               separate kernel), 1 the last split of a row block
