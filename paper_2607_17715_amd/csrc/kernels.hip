@@ -875,6 +875,14 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int v = 0; v < 16; ++v) o[db][v] = 0.f;
+  // bf16: scores leave Q K^T already relative to the reference maximum, the
+  // first MFMA of each chain adding `bias` (minus the reference, per row), so
+  // the exponentials subtract nothing; the bias changes with the (lazy)
+  // reference only.  m_biased: the reference it holds (0 while m_run is -inf).
+  f32x16 bias;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) bias[v] = 0.f;
+  float m_biased = 0.f;
 
   // ---- S^T = K Q^T over this wavefront's 32-key blocks, accumulator lane = query
   auto qk = [&](const T* sK, f32x16 (&s)[NKB]) {
@@ -892,9 +900,7 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 #pragma unroll
       for (int f = 0; f < AH; ++f) kf[f] = frag(f);
 #pragma unroll
-      for (int j = 0; j < NKB; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) s[j][v] = 0.f;
+      for (int j = 0; j < NKB; ++j) s[j] = bias;
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int f = 0; f < NF; ++f) {
@@ -906,8 +912,12 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 #pragma unroll
       for (int j = 0; j < NKB; ++j) {
         const int kb = kh * NKB + j;
+        if constexpr (KPL == 8) {
+          s[j] = bias;
+        } else {
 #pragma unroll
-        for (int v = 0; v < 16; ++v) s[j][v] = 0.f;
+          for (int v = 0; v < 16; ++v) s[j][v] = 0.f;
+        }
         const T* krow = sK + (kb * 32 + qi) * L::LDK + half * KPL;
 #pragma unroll
         for (int c = 0; c < NQC; ++c) {
@@ -997,7 +1007,7 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
           }
       }
     }
-    return fmaxf(m_run, half_pair_max(max_of(s)));
+    return fmaxf(m_run, half_pair_max(max_of(s)) + m_biased);   // absolute
   };
 
   // ---- rescale the running sum and output to a new maximum
@@ -1095,9 +1105,20 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
       // bf16: the reference maximum moves only when some row's maximum outgrows it
       // by more than kLazyLog2 (a factor 2^kLazyLog2), so the output rescale is
       // rare; probabilities stay below 2^kLazyLog2, which bf16 and fp32 sums hold
-      if (__any(m_new > m_run + kLazyLog2)) rescale(m_new, m_ref);
+      if (__any(m_new > m_run + kLazyLog2)) {
+        rescale(m_new, m_ref);
+        // re-base the scores and the bias on the new reference
+        const float d = m_ref - m_biased;
+#pragma unroll
+        for (int j = 0; j < NKB; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) s[j][v] -= d;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) bias[v] = -m_ref;
+        m_biased = m_ref;
+      }
       Op pb[NPW];
-      l_run += exp_pack(s, m_run == kNegInf ? 0.f : m_run, pb);
+      l_run += exp_pack(s, 0.f, pb);
       pv(vst(stage), pb);
     } else {
       float psum = 0.f;
