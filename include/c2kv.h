@@ -13,6 +13,18 @@
  *   - the attention of F over [KV_total, x_q] (Eq. 4)      -> `c2kv_attend`;
  *   - both at once, without materialising KV_total         -> `c2kv_compose_attend`.
  *
+ * Typical use (one batch of requests; every layer reuses the plan, since the
+ * kept sets and positions are the same for all layers and heads):
+ *   c2kv_plan_create(&cfg, &desc, suffix_len, NULL, &plan);          host, once
+ *   c2kv_plan_get_info(plan, &info);             workspace_bytes, n_pages, ...
+ *   c2kv_plan_upload(plan, workspace, info.workspace_bytes, stream); once
+ *   per layer, either
+ *     c2kv_compose_attend(plan, &pool, q, k_suf, v_suf, out, lse, stream);
+ *   or, keeping the composed cache (decode steps attend to it again):
+ *     c2kv_compose(plan, &pool, k_pages, v_pages, NULL, NULL, NULL, stream);
+ *     c2kv_attend(plan, k_pages, v_pages, q, k_suf, v_suf, out, lse, stream);
+ *   c2kv_plan_destroy(plan);
+ *
  * Conventions shared by every call
  *   Ownership.  The caller owns every buffer.  The library never allocates
  *     device memory: scratch lives in a caller-provided workspace whose size
@@ -218,7 +230,8 @@ c2kv_status c2kv_attend(const c2kv_plan* plan, const void* k_pages, const void* 
 
 /* compose + attend in one pass: the kept rows are gathered, decoded and turned
  * while they are loaded for attention, and the composed cache is never written.
- * Same result as c2kv_compose followed by c2kv_attend (up to rounding order). */
+ * Same result as c2kv_compose followed by c2kv_attend, bit for bit (both round a
+ * turned key once to the act dtype and use the same arithmetic after). */
 c2kv_status c2kv_compose_attend(const c2kv_plan* plan, const c2kv_pool* pool,
                                 const void* q, const void* k_suf, const void* v_suf,
                                 void* out, float* lse, void* stream);
