@@ -66,10 +66,14 @@ hipError_t timed(const char* name, F&& launch) {
     a = take_event();
     b = take_event();
   }
-  if (!a || !b) return hipErrorOutOfMemory;
-  hipError_t e = launch(a, b);
-  if (e != hipSuccess) return e;
+  hipError_t e = a && b ? launch(a, b) : hipErrorOutOfMemory;
   std::lock_guard<std::mutex> lk(g_timing.mu);
+  if (e != hipSuccess) {
+    // events of a launch that did not happen go back to the spare list
+    if (a) g_timing.spare.push_back(a);
+    if (b) g_timing.spare.push_back(b);
+    return e;
+  }
   g_timing.recs[name].push_back({a, b});
   return hipSuccess;
 }
