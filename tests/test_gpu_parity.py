@@ -292,3 +292,40 @@ def test_lse_optional_and_plan_reuse_across_layers():
         ref_out, ref_lse, _ = oracle_ref(w)
         lse = torch.from_numpy(ref_lse.astype(np.float32))
         compare(w, out, lse, ref_out, ref_lse, what=f"layer {l}")
+
+
+@pytest.mark.parametrize("pool_dtype", ["bf16", "i8", "f32"])
+def test_pool_rows_past_4gib(pool_dtype):
+    """Kept rows more than 4.5 GiB into the pool: the same rows moved r0 rows up
+    in a larger pool (seg_row0 shifted by r0) give bit-identical outputs, pages
+    and source rows on both paths, and the unshifted run meets the oracle."""
+    w = synth.small(pool_dtype=pool_dtype, n_q_heads=16, n_kv_heads=8, suffix_len=21)
+    n, H, D = w.pool_k.shape
+    esz = {"bf16": 2, "i8": 1, "f32": 4}[pool_dtype]
+    r0 = -(-(9 << 29) // (H * D * esz))
+    say(f"pool past 4.5 GiB {pool_dtype}: r0 = {r0} rows, {(r0 + n) * H * D * esz / 2**30:.2f} GiB")
+    ref_out, ref_lse, _ = oracle_ref(w)
+    out, lse, plan, dev = run_fused(w)
+    compare(w, out, lse, ref_out, ref_lse, what="pool4g/base")
+    out_p, lse_p, _, _, pg = run_paged(w, dev=dev, plan=plan)
+    assert torch.equal(out_p, out)
+
+    def moved(t):
+        big = torch.zeros((r0 + t.shape[0],) + tuple(t.shape[1:]), dtype=t.dtype, device="cuda")
+        big[r0:] = t
+        return big
+
+    # the descriptor holds raw pointers: keep the moved tensors referenced
+    held = [moved(dev.k), moved(dev.v), None if dev.ks is None else moved(dev.ks),
+            None if dev.vs is None else moved(dev.vs)]
+    dev.pool = c2kv.pool_desc(*held)
+    w2 = synth.with_overrides(w, seg_row0=(w.seg_row0 + r0).astype(w.seg_row0.dtype))
+    out2, lse2, plan2, _ = run_fused(w2, dev=dev)
+    assert torch.equal(out2, out) and torch.equal(lse2, lse)
+    out3, lse3, _, _, pg2 = run_paged(w2, dev=dev, plan=plan2)
+    assert torch.equal(out3, out) and torch.equal(lse3, lse_p)
+    assert torch.equal(pg2["k_pages"], pg["k_pages"]) and torch.equal(pg2["v_pages"], pg["v_pages"])
+    assert torch.equal(pg2["src"], pg["src"] + r0)
+    dev.pool = None
+    del held
+    torch.cuda.empty_cache()
