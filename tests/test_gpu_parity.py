@@ -329,3 +329,51 @@ def test_pool_rows_past_4gib(pool_dtype):
     dev.pool = None
     del held
     torch.cuda.empty_cache()
+
+
+def _replicate(w, B):
+    """B identical requests: every request repeats the segments, kept sets and
+    suffix inputs of request 0 of w (a one-request workload); the pool is shared."""
+    kept_counts = np.diff(w.seg_kept_off)
+    tile = lambda a: np.tile(a, (B,) + (1,) * (a.ndim - 1))
+    return synth.with_overrides(
+        w, req_seg_off=(np.arange(B + 1) * w.n_segments).astype(w.req_seg_off.dtype),
+        seg_row0=tile(w.seg_row0), seg_span=tile(w.seg_span),
+        seg_orig_pos0=tile(w.seg_orig_pos0),
+        seg_new_pos0=None if w.seg_new_pos0 is None else tile(w.seg_new_pos0),
+        seg_kept_off=np.concatenate([[0], np.cumsum(tile(kept_counts))]).astype(
+            w.seg_kept_off.dtype),
+        kept_idx=tile(w.kept_idx), q=tile(w.q), k_suf=tile(w.k_suf), v_suf=tile(w.v_suf))
+
+
+def test_pages_past_4gib():
+    """Composed pages more than 4 GiB into k_pages and v_pages: 36 copies of one
+    64k-token decode request, with the same key splits, each give the output of
+    the request alone bit for bit, and that output meets the oracle."""
+    sp = synth.Spec("decode-64k-pages", 32, 8, 128, 5e5, "bf16", "bf16", 8, 8192, 0, 1, 8,
+                    "natural", ("all",), 1)
+    w = synth.build(sp, seed=23)
+    assert w.batch == 1
+    ref_out, ref_lse, _ = oracle_ref(w)
+    say("pages past 4 GiB: one request")
+    out, lse, _, _, _ = run_paged(w, kv_splits=4)
+    compare(w, out, lse, ref_out, ref_lse, what="pages4g/one")
+    B = 36
+    wB = _replicate(w, B)
+    plan = c2kv.Plan.for_workload(wB, kv_splits=4).upload()
+    page_bytes = plan.info["n_pages"] * w.n_kv_heads * plan.info["page_size"] * w.head_dim * 2
+    say(f"pages past 4 GiB: {B} requests, k_pages {page_bytes / 2**30:.2f} GiB")
+    assert page_bytes > (4 << 30)
+    outB, lseB, _, _, pg = run_paged(wB, plan=plan)
+    for b in range(B):
+        assert torch.equal(outB[b], out[0]), b
+        assert torch.equal(lseB[b], lse[0]), b
+    # the last request's pages (past 4 GiB) hold what the first request's hold
+    bt = pg["bt"].cpu().numpy()
+    npg = plan.info["max_pages"]
+    assert (bt[B - 1] == bt[B - 1][0] + np.arange(npg)).all() and bt[0][0] == 0
+    last = slice(int(bt[B - 1][0]), int(bt[B - 1][0]) + npg)
+    assert torch.equal(pg["k_pages"][last], pg["k_pages"][:npg])
+    assert torch.equal(pg["v_pages"][last], pg["v_pages"][:npg])
+    del pg
+    torch.cuda.empty_cache()
