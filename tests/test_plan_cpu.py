@@ -208,3 +208,14 @@ def test_sif_row_blocks_need_no_merge():
         assert i["n_merge_groups"] == 0 and i["max_splits"] == 1, (rb, i)
     i = c2kv.Plan.for_sif(w, kv_splits=2).info
     assert i["n_merge_groups"] > 0 and i["max_splits"] >= 2
+
+
+def test_binding_refuses_to_import_without_the_library(tmp_path):
+    """No fallback: with the library missing, importing the binding raises."""
+    import subprocess
+    import sys
+    env = dict(os.environ, C2KV_LIBRARY=str(tmp_path / "missing" / "libc2kv.so"))
+    r = subprocess.run([sys.executable, "-c", "import paper_2607_17715_amd"], cwd=ROOT, env=env,
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "ImportError" in r.stderr and "is not built" in r.stderr
