@@ -159,7 +159,7 @@ def cpu_baseline(w, idx: int):
             oracle.compose_attend(w)
             reps += 1
             el = time.perf_counter() - t0
-            if el > 10.0 or reps >= 200:
+            if el > 10.0 or reps >= 5000:
                 break
         per_layer = el / reps
         sample = f"whole layer x{reps} (compose of {N} slots + attention of all {S} suffix tokens)"
