@@ -66,8 +66,13 @@
  *   - Composed slot order = segments in request order, kept indices ascending.
  *   - RoPE: theta_i = base^(-2i/D), pairs (i, i + D/2).  Softmax scale 1/sqrt(D)
  *     unless given.  Query head h reads kv-head h / (H_q / H_kv).
- *   - Suffix token t is at position span_end + t, where span_end = end of the last
- *     segment's span; it sees every composed slot and suffix tokens u <= t.
+ *   - Suffix token t is at position span_end + t, where span_end is the first
+ *     position past every placed span: the maximum over the request's segments
+ *     of new_pos0 + seg_span (with accumulated placement, the end of the last
+ *     segment's span; with explicit placements, whichever span reaches
+ *     furthest, which need not be the last segment's).  The query tokens run
+ *     after the whole composed context (Section 2.2, Eq. 4).  Suffix token t
+ *     sees every composed slot and suffix tokens u <= t.
  */
 #ifndef C2KV_H
 #define C2KV_H
@@ -130,7 +135,8 @@ typedef struct c2kv_compose_desc {
   const int32_t* req_seg_off;    /* [B+1] CSR: segments of request b are
                                     req_seg_off[b] .. req_seg_off[b+1]-1, in order  */
   const int64_t* seg_row0;       /* [n_segments] pool row of the segment's token 0  */
-  const int32_t* seg_span;       /* [n_segments] uncompressed length n (>= 1)       */
+  const int32_t* seg_span;       /* [n_segments] uncompressed length n (>= 1;
+                                    C2KV_E_INVAL otherwise)                         */
   const int32_t* seg_orig_pos0;  /* [n_segments] position token 0 was encoded at    */
   const int32_t* seg_new_pos0;   /* [n_segments] placement, or NULL: span-preserving
                                     accumulation from 0 within each request         */

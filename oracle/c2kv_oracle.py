@@ -29,7 +29,11 @@ Readings where the paper is silent (each is listed in the design notes):
   * RoPE uses theta_i = base^(-2i/d) with half-split pairing (i, i + d/2);
   * softmax scale 1/sqrt(d); query head h reads kv-head h // (H_q / H_kv);
   * suffix token t sits at position span_end + t, sees every composed slot and
-    suffix tokens u <= t; span_end = end of the last segment's span;
+    suffix tokens u <= t; span_end = the first position past every placed span
+    (the maximum of new_pos0 + span over the request's segments: the end of the
+    last span under accumulated placement, and of the furthest one when
+    placements are given explicitly), since the query tokens run after the
+    whole composed context (Section 2.2, Eq. 4);
   * lse is the natural-log log-sum-exp of the scaled scores.
 
 Parity: pinned by the CPU tests (worked layout examples, RoPE group laws and
@@ -116,7 +120,9 @@ def compose_layout(req_seg_off, seg_row0, seg_span, seg_orig_pos0, seg_kept_off,
     (ascending) becomes a slot with
         src_row = row0_c + j,  p_orig = orig_pos0_c + j,
         p_new   = new_pos0_c + j,  delta = new_pos0_c - orig_pos0_c.
-    span_end of the request = start of the first position after its last span.
+    span_end of the request = the first position past every span: the maximum
+    of new_pos0_c + span_c over its segments (with explicit placements the
+    furthest span need not be the last segment's).  Spans are >= 1.
     Slot order = segments in request order, then kept indices ascending.
     compressed=True reads a pool that stores each chunk compressed (only its
     kept tokens, in order): the k-th kept token of a segment is row row0_c + k.

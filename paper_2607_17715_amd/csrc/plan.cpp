@@ -159,7 +159,7 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       const int64_t row0 = d.seg_row0[c];
       const int64_t orig0 = d.seg_orig_pos0[c];
       const int64_t new0 = d.seg_new_pos0 ? int64_t(d.seg_new_pos0[c]) : cursor;
-      if (span < 0) { err = fmt("seg_span[", c, "] < 0"); return C2KV_E_INVAL; }
+      if (span < 1) { err = fmt("seg_span[", c, "] must be >= 1, got ", span); return C2KV_E_INVAL; }
       if (row0 < 0) { err = fmt("seg_row0[", c, "] < 0"); return C2KV_E_INVAL; }
       if (orig0 < 0 || new0 < 0) { err = fmt("negative position at segment ", c); return C2KV_E_INVAL; }
       const int64_t delta = new0 - orig0;
@@ -193,6 +193,8 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
       }
       if (first_row >= 0) p.load_rows.push_back({first_row, last_row + 1});
       cursor = new0 + span;               // span-preserving: advance by n, not m
+      // the query tokens start past every placed span (explicit placements may
+      // put the furthest span before the last segment)
       end = std::max(end, new0 + span);
     }
     if (end + suffix_len - 1 > kI32Max) {

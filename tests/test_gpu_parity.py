@@ -54,7 +54,13 @@ def test_long_suffix_sampled_rows():
     """Full 70B-shaped workload (32768 composed slots, S = 2048) in the launch
     configuration the benchmark times; the oracle computes sampled suffix rows."""
     w = synth.config(5)
-    rows = [0, 1, 63, 64, 65, 1000, 1023, 1024, 2046, 2047]
+    # one suffix token in each of the 64 row blocks of 256 rows (32 tokens of 8
+    # heads each), at a different offset in each block so that every in-block
+    # position of the causal diagonal tile is met, plus both ends
+    G = w.n_q_heads // w.n_kv_heads
+    per_block = 256 // G
+    rows = sorted({0, 1, w.suffix_len - 1} |
+                  {per_block * i + (i % per_block) for i in range(w.suffix_len // per_block)})
     _both_paths(w, "70b-long-suffix", rows=rows)
 
 
@@ -271,6 +277,26 @@ def test_repeated_chunks_and_explicit_placement():
         kept_idx=np.concatenate([np.arange(0, 140, 2), np.arange(5), np.arange(0, 140, 2)]
                                 ).astype(np.int32))
     _both_paths(w, "repeated chunk, explicit placement")
+
+
+def test_explicit_placement_golden():
+    """The hand-worked explicit-placement layout (out of order, overlapping, a
+    segment that keeps nothing, negative deltas; the furthest span is not the
+    last segment's), end to end through both paths against the oracle."""
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                    "layout_explicit_placement.json")))
+    w = synth.small(batch=2, suffix_len=19)
+    a = lambda k, t: np.array(g[k], t)
+    w = synth.with_overrides(
+        w, req_seg_off=a("req_seg_off", np.int32), seg_row0=a("seg_row0", np.int64),
+        seg_span=a("seg_span", np.int32), seg_orig_pos0=a("seg_orig_pos0", np.int32),
+        seg_new_pos0=a("seg_new_pos0", np.int32), seg_kept_off=a("seg_kept_off", np.int32),
+        kept_idx=a("kept_idx", np.int32))
+    plan = _both_paths(w, "explicit placement golden")
+    n, e = plan.requests()
+    assert list(e) == g["expect"]["span_end"]
 
 
 def test_gqa_groups():

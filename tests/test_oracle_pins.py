@@ -37,6 +37,48 @@ def test_layout_worked_example():
     assert list(map(int, lay["composed_len"])) == g["expect"]["composed_len"]
 
 
+def test_layout_explicit_placement_worked_example():
+    """Explicit placements out of order and overlapping, one segment keeping
+    nothing, negative deltas: the hand-worked values, including span_end as the
+    first position past every placed span (not the last segment's span end)."""
+    g = json.load(open(os.path.join(GOLDEN, "layout_explicit_placement.json")))
+    lay = oracle.compose_layout(g["req_seg_off"], g["seg_row0"], g["seg_span"],
+                                g["seg_orig_pos0"], g["seg_kept_off"], g["kept_idx"],
+                                seg_new_pos0=g["seg_new_pos0"])
+    for key in ("src_row", "p_new", "p_orig", "delta", "seg"):
+        got = [list(map(int, a)) for a in lay[key]]
+        assert got == g["expect"][key], key
+    assert list(map(int, lay["span_end"])) == g["expect"]["span_end"]
+    assert list(map(int, lay["composed_len"])) == g["expect"]["composed_len"]
+    # the case the pin exists for: the last segment is not the furthest
+    assert g["expect"]["span_end"] != g["expect"]["last_segment_span_end"]
+
+
+def test_span_end_is_past_every_covered_position():
+    """Independent construction of span_end for explicit placements: mark every
+    position that any segment's uncompressed span covers, token by token; the
+    first query position is one past the largest marked position, and no cached
+    slot sits at or after it."""
+    rng = np.random.default_rng(77)
+    for _ in range(200):
+        nseg = int(rng.integers(1, 6))
+        span = rng.integers(1, 9, nseg)
+        new0 = rng.integers(0, 40, nseg)
+        kept = [np.sort(rng.choice(int(s), size=int(rng.integers(0, s + 1)), replace=False))
+                for s in span]
+        koff = np.concatenate([[0], np.cumsum([len(k) for k in kept])])
+        lay = oracle.compose_layout([0, nseg], np.zeros(nseg, int), span,
+                                    np.zeros(nseg, int), koff,
+                                    np.concatenate(kept + [np.zeros(0, int)]),
+                                    seg_new_pos0=new0)
+        covered = set()
+        for c in range(nseg):
+            covered.update(range(int(new0[c]), int(new0[c] + span[c])))
+        expect = max(covered) + 1
+        assert int(lay["span_end"][0]) == expect
+        assert all(int(p) < expect for p in lay["p_new"][0])
+
+
 def _layout_by_loops(w):
     """Second, independent enumeration: positions from a running cursor over
     every uncompressed token of every segment (kept or not)."""

@@ -2,6 +2,7 @@
 include/c2kv.h declares; the plan's kept-token layout equals the oracle's
 bit for bit; bad descriptors are rejected with the documented status codes."""
 import ctypes
+import json
 import os
 import re
 
@@ -81,6 +82,48 @@ def test_layout_explicit_placement_and_repeats():
     _assert_layout_equal(w, plan)
     n, e = plan.requests()
     assert e[0] == 5200
+
+
+def _golden_workload(name):
+    """A small workload whose layout is the hand-worked golden `name` (pool values
+    from the seeded generator; the golden's rows all lie inside its pool)."""
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", name)))
+    w = synth.small(batch=len(g["req_seg_off"]) - 1, suffix_len=19)
+    a = lambda k, t: None if g.get(k) is None else np.array(g[k], t)
+    return g, synth.with_overrides(
+        w, req_seg_off=a("req_seg_off", np.int32), seg_row0=a("seg_row0", np.int64),
+        seg_span=a("seg_span", np.int32), seg_orig_pos0=a("seg_orig_pos0", np.int32),
+        seg_new_pos0=a("seg_new_pos0", np.int32), seg_kept_off=a("seg_kept_off", np.int32),
+        kept_idx=a("kept_idx", np.int32))
+
+
+@pytest.mark.parametrize("name", ["layout_worked_example.json", "layout_explicit_placement.json"])
+def test_plan_layout_matches_hand_worked_golden(name):
+    """The plan builder's slot table and span ends against the values worked by
+    hand (the explicit-placement golden has its furthest span on a segment that
+    is not the last)."""
+    g, w = _golden_workload(name)
+    plan = c2kv.Plan.for_workload(w)
+    n, e = plan.requests()
+    assert list(n) == g["expect"]["composed_len"]
+    assert list(e) == g["expect"]["span_end"]
+    src, pos, dl = plan.slots()
+    assert list(src) == [x for r in g["expect"]["src_row"] for x in r]
+    assert list(pos) == [x for r in g["expect"]["p_new"] for x in r]
+    assert list(dl) == [x for r in g["expect"]["delta"] for x in r]
+
+
+def test_zero_span_is_rejected():
+    w = synth.small(batch=1, chunks_per_req=2, prefix_len=0)
+    span = w.seg_span.copy()
+    span[1] = 0
+    kept_off = w.seg_kept_off.copy()
+    kept_off[2] = kept_off[1]
+    w = synth.with_overrides(w, seg_span=span, seg_kept_off=kept_off,
+                             kept_idx=w.kept_idx[:kept_off[1]])
+    with pytest.raises(c2kv.C2KVError) as ei:
+        c2kv.Plan.for_workload(w)
+    assert ei.value.status == c2kv.C2KV_E_INVAL and "seg_span" in str(ei.value)
 
 
 def test_block_table_pages():
