@@ -1,6 +1,8 @@
 """Build libc2kv.so (HIP kernels + host plan + C ABI) for gfx950 with hipcc.
 
-    python -m paper_2607_17715_amd.build        # builds in-tree
+    python paper_2607_17715_amd/build.py        # builds in-tree
+
+(run by path: `python -m` would import the package, which loads the library)
 """
 from __future__ import annotations
 
