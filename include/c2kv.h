@@ -242,6 +242,28 @@ c2kv_status c2kv_compose_attend(const c2kv_plan* plan, const c2kv_pool* pool,
                                 const void* q, const void* k_suf, const void* v_suf,
                                 void* out, float* lse, void* stream);
 
+/* Bytes of the static scratch array that c2kv_compose_attend_static uses on each
+ * GPU (held from the library's load until the process ends). */
+#define C2KV_STATIC_SCRATCH_BYTES (32u << 20)
+
+/* For callers that cannot allocate device memory or bind a workspace: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.  The
+ * same computation as c2kv_compose_attend, bit for bit (the same kernels), but
+ * the plan's tables and the key-split partials live in a static device array of
+ * C2KV_STATIC_SCRATCH_BYTES on the current GPU instead of a caller workspace; the
+ * plan need not be uploaded.  The call copies the plan's tables into the array
+ * on `stream` (which must belong to the current GPU), then launches.  It calls
+ * no hipMalloc, hipFree or other allocating routine.
+ *   C2KV_E_WORKSPACE  the plan's workspace_bytes exceed C2KV_STATIC_SCRATCH_BYTES
+ *                     (checked before any device work);
+ *   otherwise the errors of c2kv_compose_attend.
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents: calls that overlap on one GPU (other streams, other threads) race
+ * and must be ordered by the caller. */
+c2kv_status c2kv_compose_attend_static(const c2kv_plan* plan, const c2kv_pool* pool,
+                                       const void* q, const void* k_suf, const void* v_suf,
+                                       void* out, float* lse, void* stream);
+
 /* Extraction-time attention with Structured Information Flow (Section 3.3):
  * each of `batch` sequences holds n_tokens original tokens followed by one C^2
  * token per block of `block` originals, m = ceil(n_tokens / block) of them.  The

@@ -30,8 +30,9 @@ EXPORTED = [
     "c2kv_plan_get_slots", "c2kv_plan_get_block_table", "c2kv_plan_upload", "c2kv_compose",
     "c2kv_attend", "c2kv_compose_attend", "c2kv_timing_enable", "c2kv_timing_reset",
     "c2kv_timing_read", "c2kv_last_error", "c2kv_version", "c2kv_host_alloc",
-    "c2kv_host_free", "c2kv_load", "c2kv_sif_plan_create",
+    "c2kv_host_free", "c2kv_load", "c2kv_sif_plan_create", "c2kv_compose_attend_static",
 ]
+STATIC_SCRATCH_BYTES = 32 << 20   # C2KV_STATIC_SCRATCH_BYTES
 
 
 class C2KVError(RuntimeError):
@@ -82,7 +83,7 @@ class PlanInfo(ctypes.Structure):
 
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_17715_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2607_17715_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     P = ctypes.POINTER
@@ -97,6 +98,7 @@ def _load() -> ctypes.CDLL:
         "c2kv_compose": [vp, P(PoolDesc), vp, vp, vp, vp, vp, vp],
         "c2kv_attend": [vp, vp, vp, vp, vp, vp, vp, vp, vp],
         "c2kv_compose_attend": [vp, P(PoolDesc), vp, vp, vp, vp, vp, vp],
+        "c2kv_compose_attend_static": [vp, P(PoolDesc), vp, vp, vp, vp, vp, vp],
         "c2kv_timing_enable": [i32],
         "c2kv_timing_reset": [],
         "c2kv_timing_read": [ctypes.c_char_p, P(ctypes.c_double), P(i64)],
@@ -310,6 +312,15 @@ def c2kv_compose_attend(plan: Plan, pool: PoolDesc, q, k_suf, v_suf, out, lse=No
     _check(_lib.c2kv_compose_attend(plan.handle, ctypes.byref(pool), _dev_ptr(q),
                                     _dev_ptr(k_suf), _dev_ptr(v_suf), _dev_ptr(out),
                                     _dev_ptr(lse), _stream(stream)))
+
+
+def c2kv_compose_attend_static(plan: Plan, pool: PoolDesc, q, k_suf, v_suf, out, lse=None,
+                               stream=None):
+    """c2kv_compose_attend with the tables and partials in the library's static
+    device array (no workspace, no upload needed)."""
+    _check(_lib.c2kv_compose_attend_static(plan.handle, ctypes.byref(pool), _dev_ptr(q),
+                                           _dev_ptr(k_suf), _dev_ptr(v_suf), _dev_ptr(out),
+                                           _dev_ptr(lse), _stream(stream)))
 
 
 def c2kv_load(plan: Plan, src: PoolDesc, dst: PoolDesc, stream=None):

@@ -258,8 +258,8 @@ c2kv_status c2kv_compose(const c2kv_plan* plan, const c2kv_pool* pool, void* k_p
     return fail(C2KV_E_INVAL, "k_pages and v_pages must not be NULL");
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = timed("compose", [&](hipEvent_t e0, hipEvent_t e1) {
-    return c2kv::launch_compose(p, pool->dtype, pool->k, pool->v, pool->k_scale, pool->v_scale,
-                                k_pages, v_pages, slot_src_row, slot_pos, s, e0, e1);
+    return c2kv::launch_compose(p, p.d_workspace, pool->dtype, pool->k, pool->v, pool->k_scale,
+                                pool->v_scale, k_pages, v_pages, slot_src_row, slot_pos, s, e0, e1);
   });
   if (e != hipSuccess) return hip_fail(e, "compose launch");
   if (block_table) {
@@ -271,19 +271,19 @@ c2kv_status c2kv_compose(const c2kv_plan* plan, const c2kv_pool* pool, void* k_p
   return C2KV_OK;
 }
 
-static c2kv_status run_attention(const c2kv::Plan& p, int src_kind, const char* name,
+static c2kv_status run_attention(const c2kv::Plan& p, void* ws, int src_kind, const char* name,
                                  const void* k, const void* v, const float* ks,
                                  const float* vs, const void* q, const void* k_suf,
                                  const void* v_suf, void* out, float* lse, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e = timed(name, [&](hipEvent_t e0, hipEvent_t e1) {
-    return c2kv::launch_attention(p, src_kind, k, v, ks, vs, q, k_suf, v_suf, out, lse, s, e0,
+    return c2kv::launch_attention(p, ws, src_kind, k, v, ks, vs, q, k_suf, v_suf, out, lse, s, e0,
                                   e1);
   });
   if (e != hipSuccess) return hip_fail(e, "attention launch");
   if (!p.merges.empty() && !p.merge_in_kernel) {
     e = timed("merge", [&](hipEvent_t e0, hipEvent_t e1) {
-      return c2kv::launch_merge(p, out, lse, s, e0, e1);
+      return c2kv::launch_merge(p, ws, out, lse, s, e0, e1);
     });
     if (e != hipSuccess) return hip_fail(e, "merge launch");
   }
@@ -299,8 +299,8 @@ c2kv_status c2kv_attend(const c2kv_plan* plan, const void* k_pages, const void* 
   const c2kv::Plan& p = plan->p;
   if ((!k_pages || !v_pages) && p.n_pages > 0)
     return fail(C2KV_E_INVAL, "k_pages and v_pages must not be NULL");
-  return run_attention(p, c2kv::kSrcPaged, "attn_paged", k_pages, v_pages, nullptr, nullptr,
-                       q, k_suf, v_suf, out, lse, stream);
+  return run_attention(p, p.d_workspace, c2kv::kSrcPaged, "attn_paged", k_pages, v_pages,
+                       nullptr, nullptr, q, k_suf, v_suf, out, lse, stream);
 }
 
 c2kv_status c2kv_compose_attend(const c2kv_plan* plan, const c2kv_pool* pool, const void* q,
@@ -312,8 +312,35 @@ c2kv_status c2kv_compose_attend(const c2kv_plan* plan, const c2kv_pool* pool, co
   if (!check_pool(p, pool, &st)) return st;
   if (!check_io(q, k_suf, v_suf, out, &st)) return st;
   const int kind = pool->dtype == C2KV_I8 ? c2kv::kSrcPoolI8 : c2kv::kSrcPool;
-  return run_attention(p, kind, "attn_pool", pool->k, pool->v, pool->k_scale, pool->v_scale,
-                       q, k_suf, v_suf, out, lse, stream);
+  return run_attention(p, p.d_workspace, kind, "attn_pool", pool->k, pool->v, pool->k_scale,
+                       pool->v_scale, q, k_suf, v_suf, out, lse, stream);
+}
+
+c2kv_status c2kv_compose_attend_static(const c2kv_plan* plan, const c2kv_pool* pool,
+                                       const void* q, const void* k_suf, const void* v_suf,
+                                       void* out, float* lse, void* stream) {
+  if (!plan) return fail(C2KV_E_INVAL, "plan is NULL");
+  const c2kv::Plan& p = plan->p;
+  // checked before any HIP call: the tables and partials must fit the array
+  if (p.ws.total > C2KV_STATIC_SCRATCH_BYTES)
+    return fail(C2KV_E_WORKSPACE,
+                "plan needs " + std::to_string(p.ws.total) + " bytes of scratch; the static "
+                "array holds " + std::to_string(size_t(C2KV_STATIC_SCRATCH_BYTES)) +
+                " (use c2kv_compose_attend with a workspace)");
+  c2kv_status st;
+  if (!check_pool(p, pool, &st)) return st;
+  if (!check_io(q, k_suf, v_suf, out, &st)) return st;
+  void* ws = nullptr;
+  hipError_t e = c2kv::static_scratch(&ws);
+  if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (static scratch)");
+  // this call's tables, over whatever the last call on this GPU left; the image
+  // carries the zeroed merge counters as well
+  e = hipMemcpyAsync(ws, p.image.data(), p.image.size(), hipMemcpyHostToDevice,
+                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (tables into static scratch)");
+  const int kind = pool->dtype == C2KV_I8 ? c2kv::kSrcPoolI8 : c2kv::kSrcPool;
+  return run_attention(p, ws, kind, "attn_pool", pool->k, pool->v, pool->k_scale,
+                       pool->v_scale, q, k_suf, v_suf, out, lse, stream);
 }
 
 c2kv_status c2kv_host_alloc(size_t bytes, void** host, void** device) {

@@ -20,6 +20,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <type_traits>
 
 #include "plan.hpp"
@@ -1622,6 +1623,34 @@ __global__ __launch_bounds__(256) void compose_kernel(ComposeParams a) {
 // launchers
 // ----------------------------------------------------------------------------
 
+// ----------------------------------------------------------------------------
+// static scratch of the allocation-free entry point
+// ----------------------------------------------------------------------------
+
+// One array per GPU (each device holds its own copy, at its own address, until
+// the process ends).  Host code never passes the array's name to a kernel or a
+// copy: in host code it is only a stand-in, so its device address is looked up.
+static __device__ __align__(256) unsigned char scratch[C2KV_STATIC_SCRATCH_BYTES];
+
+hipError_t static_scratch(void** out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = a;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
+
 namespace {
 
 // Launch `kernel(params)`.  With timing events, the dispatch packet itself
@@ -1664,11 +1693,10 @@ hipError_t launch_attn_d(int D, const AttnParams& ap, int n, int rows, hipStream
 
 }  // namespace
 
-hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const void* v,
+hipError_t launch_attention(const Plan& p, void* ws, int src_kind, const void* k, const void* v,
                             const float* k_scale, const float* v_scale, const void* q,
                             const void* k_suf, const void* v_suf, void* out, float* lse,
                             hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
-  void* ws = p.d_workspace;
   AttnParams ap{};
   ap.Hq = p.cfg.n_q_heads;
   ap.Hkv = p.cfg.n_kv_heads;
@@ -1720,17 +1748,17 @@ hipError_t launch_attention(const Plan& p, int src_kind, const void* k, const vo
   return launch_attn_d<__bf16, SRC_POOL_I8>(D, ap, n, rows, st, e0, e1);
 }
 
-hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st, hipEvent_t e0,
-                        hipEvent_t e1) {
+hipError_t launch_merge(const Plan& p, void* ws, void* out, float* lse, hipStream_t st,
+                        hipEvent_t e0, hipEvent_t e1) {
   if (p.merges.empty() || p.merge_in_kernel) return hipSuccess;
   MergeParams mp{};
   mp.Hq = p.cfg.n_q_heads;
   mp.G = p.group;
   mp.S = p.suffix_len;
   mp.RB = p.rows_per_block;
-  mp.groups = at<MergeGroup>(p.d_workspace, p.ws.merges);
-  mp.part_o = at<unsigned char>(p.d_workspace, p.ws.part_o);
-  mp.part_lse = at<float>(p.d_workspace, p.ws.part_lse);
+  mp.groups = at<MergeGroup>(ws, p.ws.merges);
+  mp.part_o = at<unsigned char>(ws, p.ws.part_o);
+  mp.part_lse = at<float>(ws, p.ws.part_lse);
   mp.out = out;
   mp.lse = lse;
   const int D = p.cfg.head_dim;
@@ -1759,7 +1787,7 @@ hipError_t launch_merge(const Plan& p, void* out, float* lse, hipStream_t st, hi
   return launch(k, grid, dim3(256), st, mp, e0, e1);
 }
 
-hipError_t launch_compose(const Plan& p, int pool_dtype, const void* k, const void* v,
+hipError_t launch_compose(const Plan& p, void* ws, int pool_dtype, const void* k, const void* v,
                           const float* k_scale, const float* v_scale, void* k_pages,
                           void* v_pages, int64_t* out_src_row, int32_t* out_pos,
                           hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
@@ -1768,10 +1796,10 @@ hipError_t launch_compose(const Plan& p, int pool_dtype, const void* k, const vo
   ComposeParams cp{};
   cp.Hkv = p.cfg.n_kv_heads;
   cp.PS = p.page_size;
-  cp.slot_info = at<int2>(p.d_workspace, p.ws.slot_info);
-  cp.slot_pos = at<int>(p.d_workspace, p.ws.slot_pos);
-  cp.seg_cs = at<float2>(p.d_workspace, p.ws.seg_cs);
-  cp.tiles = at<int4>(p.d_workspace, p.ws.compose_tiles);
+  cp.slot_info = at<int2>(ws, p.ws.slot_info);
+  cp.slot_pos = at<int>(ws, p.ws.slot_pos);
+  cp.seg_cs = at<float2>(ws, p.ws.seg_cs);
+  cp.tiles = at<int4>(ws, p.ws.compose_tiles);
   cp.k = k;
   cp.v = v;
   cp.k_scale = k_scale;

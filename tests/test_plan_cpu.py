@@ -126,6 +126,20 @@ def test_zero_span_is_rejected():
     assert ei.value.status == c2kv.C2KV_E_INVAL and "seg_span" in str(ei.value)
 
 
+def test_static_entry_rejects_plans_beyond_its_array():
+    """c2kv_compose_attend_static refuses a plan whose tables and partials exceed
+    the static array, before any device work (so this runs without a GPU)."""
+    w = synth.small(batch=4, n_q_heads=32, n_kv_heads=8, suffix_len=64, keep=("all",),
+                    chunk_len=1000, chunks_per_req=5)
+    plan = c2kv.Plan.for_workload(w, kv_splits=64, rows_per_block=256)
+    assert plan.info["workspace_bytes"] > c2kv.STATIC_SCRATCH_BYTES
+    pool = c2kv.PoolDesc(c2kv.C2KV_BF16, 16, 16, None, None, 1 << 20)
+    st = c2kv.lib().c2kv_compose_attend_static(plan.handle, ctypes.byref(pool), 16, 16, 16, 16,
+                                               None, None)
+    assert st == c2kv.C2KV_E_WORKSPACE
+    assert b"static" in c2kv.lib().c2kv_last_error()
+
+
 def test_block_table_pages():
     w = synth.small(batch=3, keep=("ratio", 0.2, 0.9))
     for ps in (64, 128, 256):
