@@ -1,12 +1,19 @@
 """Benchmark of the C2KV compose-and-attend hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload llama3-8b-layer-bf16]
+    python bench.py [--steps K] [--warmup W] [--workload 70b-long-suffix-bf16]
 
 A step is one pass of the path over one layer of a synthetic workload:
 c2kv_compose_attend (gather, decode, re-rotate, suffix RoPE, split-K attention
 and merge) for the short-suffix workloads, c2kv_compose then c2kv_attend for
-the long-suffix one.  The plan (host layout, built once per batch of requests
-and shared by all layers) is built and uploaded before the timed region.
+the long-suffix one.  The int8 workload's step is its 32 layers back to back,
+each with its own independently seeded cache and suffix (one shared plan), and
+reports per layer.  The plan (host layout, built once per batch of requests and
+shared by all layers) is built and uploaded before the timed region.
+
+The default workload is the largest single-GPU one (the 70B-shaped long
+suffix); the same run also times the tiny fp32, Llama-3-8B layer, ragged batch
+and 32-layer int8 workloads and reports them under "configs" in the same line
+(--no-configs skips them).
 
 Inputs live in HBM before timing starts.  Steps rotate over enough device
 copies of the inputs that their footprint exceeds twice the 256 MB Infinity
@@ -64,7 +71,10 @@ for _i, (_ctx, _r) in enumerate(synth.DECODE_GRID):
     WORKLOADS[f"decode-{_ctx}k-{_r}x-bf16"] = 12 + _i
 # extraction-time attention with Structured Information Flow over document chunks
 SIF = {"sif-extract-llama3-8b-bf16"}
-DEFAULT_WORKLOAD = "llama3-8b-layer-bf16"
+DEFAULT_WORKLOAD = "70b-long-suffix-bf16"
+# timed in the same run as the default workload, reported under "configs"
+SECONDARY = ["tiny-fp32", "llama3-8b-layer-bf16", "ragged-batch-bf16", "int8-32layer"]
+SECONDARY_STEPS, SECONDARY_WARMUP = 256, 16
 LONG_SUFFIX = {"70b-long-suffix-bf16"}
 # one generated token over a cache composed once beforehand: the step is c2kv_attend
 DECODE = {name for name, idx in WORKLOADS.items() if 6 <= idx <= 9 or idx >= 12}
@@ -140,14 +150,21 @@ def load_traffic(workload: str, kernel: str, n_launch_bytes: float):
     return t.get("hbm_bytes_per_launch")
 
 
+def host_threads():
+    """(cores this process may run on, the BLAS library's thread count)."""
+    cores = len(os.sched_getaffinity(0))
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas = None
+    return cores, blas
+
+
 def cpu_baseline(w, idx: int):
     """The float64 oracle timed on this host on a bounded sample of the workload."""
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
+    cores, blas = host_threads()
     lay = oracle.compose_layout(w.req_seg_off, w.seg_row0, w.seg_span, w.seg_orig_pos0,
                                 w.seg_kept_off, w.kept_idx, w.seg_new_pos0)
     N = int(lay["composed_len"].sum())
@@ -165,30 +182,35 @@ def cpu_baseline(w, idx: int):
         sample = f"whole layer x{reps} (compose of {N} slots + attention of all {S} suffix tokens)"
     else:
         # compose every kept token of the first request(s), attention of a few suffix rows,
-        # scaled to the whole layer
+        # repeated for about 10 s, scaled to the whole layer
         reqs = list(range(min(w.batch, 2)))
         rows = list(range(0, S, max(1, S // 8)))[:8]
-        t0 = time.perf_counter()
-        oracle.compose_attend(w, rows=rows, requests=reqs)
-        el = time.perf_counter() - t0
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oracle.compose_attend(w, rows=rows, requests=reqs)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el > 10.0 or reps >= 1000:
+                break
         frac_req = float(lay["composed_len"][reqs].sum() + len(reqs)) / float(N + w.batch)
-        per_layer = el / frac_req * (S / len(rows))
+        per_layer = el / reps / frac_req * (S / len(rows))
         sample = (f"requests {reqs} ({int(lay['composed_len'][reqs].sum())} slots composed), "
-                  f"{len(rows)} of {S} suffix rows; scaled by suffix rows and by slots")
-    return {"value": N / per_layer, "unit": "tokens/s/layer", "cores": int(threads),
-            "kind": "oracle", "sample": sample, "seconds_per_layer": per_layer}
+                  f"{len(rows)} of {S} suffix rows, x{reps}; scaled by suffix rows and by slots")
+    return {"value": N / per_layer, "unit": "tokens/s/layer", "cores": cores,
+            "blas_threads": blas, "kind": "oracle", "sample": sample,
+            "seconds_per_layer": per_layer}
 
 
-def time_steps(step, copies, args, c2kv, torch):
+def time_steps(step, copies, args, c2kv, torch, steps=None, warmup=None, launches_per_step=1):
     """Warm-up, an eager timing, the timed graph replays (K steps captured over the
     input copies), and a pass with per-kernel dispatch-stamped events.  Returns
     (ms per step, eager ms per step, per-kernel averages, whether graphs ran)."""
-    for i in range(args.warmup):
+    K = args.steps if steps is None else steps
+    for i in range(args.warmup if warmup is None else warmup):
         step(i)
     torch.cuda.synchronize()
-    K = args.steps
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ke = min(K, 256)
+    ke = max(1, min(K, 256 // launches_per_step))
     torch.cuda.synchronize()
     start.record()
     for i in range(ke):
@@ -308,15 +330,202 @@ def run_sif(args, c2kv, synth, torch):
             el = time.perf_counter() - t0
             if el > 10.0 or reps >= 4 * B:
                 break
-        try:
-            from threadpoolctl import threadpool_info
-            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        except Exception:
-            threads = 1
+        cores, blas = host_threads()
         result["cpu_baseline"] = {"value": reps * L / el, "unit": "tokens/s/layer",
-                                  "cores": int(threads), "kind": "oracle",
+                                  "cores": cores, "blas_threads": blas, "kind": "oracle",
                                   "sample": f"{reps} whole sequences of {L} tokens"}
     print(json.dumps(result), flush=True)
+
+
+def run_workload(name, args, c2kv, torch, steps, warmup, with_cpu):
+    """Time one workload (not SIF); returns its result object (the JSON line's
+    fields, without the headline-only keys)."""
+    idx = WORKLOADS[name]
+    log(f"workload {name}: generating inputs")
+    sp = synth.spec(idx)
+    w = synth.config(idx)
+    layers = sp.layers if name == "int8-32layer" else 1
+    host_mode = ("zerocopy" if name in HOST_ZEROCOPY else
+                 "load" if name in HOST_LOAD else None)
+    if host_mode:
+        w = synth.compress_pool(w)
+    plan = c2kv.Plan.for_workload(w, kv_splits=args.kv_splits,
+                                  rows_per_block=args.rows_per_block,
+                                  merge_mode=args.merge_mode).upload()
+    composed, span_end = plan.requests()
+    work = algorithmic_work(w, composed)
+    long_suffix = name in LONG_SUFFIX
+    decode = name in DECODE
+    paged = long_suffix or decode
+    act = torch.float32 if w.act_dtype == "f32" else torch.bfloat16
+
+    def out_lse(s):
+        s["out"] = torch.empty_like(s["q"])
+        s["lse"] = torch.empty((w.batch, w.n_q_heads, w.suffix_len), dtype=torch.float32,
+                               device="cuda")
+        return s
+
+    if layers > 1:
+        # every layer its own seeded cache and suffix, drawn on the device; one plan
+        sets = []
+        for layer in range(layers):
+            d = synth.int8_layer_device(sp, layer, synth.BASE_SEED + idx)
+            d["ks"], d["vs"] = d.pop("k_scale"), d.pop("v_scale")
+            d["pool"] = c2kv.pool_desc(d["k"], d["v"], d["ks"], d["vs"])
+            sets.append(out_lse(d))
+        torch.cuda.synchronize()
+        copies = 1
+        log(f"{layers} layers drawn on the device; the step runs them back to back")
+
+        def step(i):
+            for s in sets:
+                c2kv.c2kv_compose_attend(plan, s["pool"], s["q"], s["k_suf"], s["v_suf"],
+                                         s["out"], s["lse"])
+    else:
+        # ---- device inputs, replicated so the rotation spans > 2x the Infinity Cache
+        base = dict(k=c2kv.to_device(w.pool_k, w.pool_dtype),
+                    v=c2kv.to_device(w.pool_v, w.pool_dtype),
+                    ks=None if w.pool_k_scale is None else c2kv.to_device(w.pool_k_scale, "f32"),
+                    vs=None if w.pool_v_scale is None else c2kv.to_device(w.pool_v_scale, "f32"),
+                    q=c2kv.to_device(w.q, w.act_dtype), k_suf=c2kv.to_device(w.k_suf, w.act_dtype),
+                    v_suf=c2kv.to_device(w.v_suf, w.act_dtype))
+        if paged:
+            ksh, vsh = c2kv.page_shapes(plan)
+        if decode:
+            # the step reads the composed pages; each copy gets its own
+            footprint = 2 * math.prod(ksh) * (4 if act == torch.float32 else 2)
+        else:
+            footprint = sum(t.numel() * t.element_size() for t in base.values() if t is not None)
+        copies = args.copies or int(min(64, max(2, math.ceil(2.2 * MALL_BYTES / footprint))))
+        log(f"footprint {footprint / 1e6:.1f} MB per copy, {copies} copies")
+        if host_mode:
+            # host memory is not cached on the device side: two copies, each with its
+            # own device pool (the load destination)
+            copies = args.copies or 2
+            hosts = [c2kv.HostPool(w.pool_k, w.pool_v, w.pool_dtype, w.pool_k_scale,
+                                   w.pool_v_scale) for _ in range(copies)]
+            sets = [base] + [{k: (None if t is None else t.clone()) for k, t in base.items()}
+                             for _ in range(copies - 1)]
+            for s, h in zip(sets, hosts):
+                s["host"] = h.desc
+            log(f"host pools: {copies} x {hosts[0].nbytes / 1e6:.1f} MB page-locked")
+        elif decode:
+            sets = [dict(base) for _ in range(copies)]          # pool shared: composed once per copy
+        else:
+            sets = [base] + [{k: (None if t is None else t.clone()) for k, t in base.items()}
+                             for _ in range(copies - 1)]
+        for s in sets:
+            s["pool"] = c2kv.pool_desc(s["k"], s["v"], s["ks"], s["vs"])
+            out_lse(s)
+        if long_suffix:
+            kp = torch.empty(ksh, dtype=act, device="cuda")
+            vp = torch.empty(vsh, dtype=act, device="cuda")
+        if decode:
+            for s in sets:
+                s["kp"] = torch.empty(ksh, dtype=act, device="cuda")
+                s["vp"] = torch.empty(vsh, dtype=act, device="cuda")
+                c2kv.c2kv_compose(plan, s["pool"], s["kp"], s["vp"])
+            torch.cuda.synchronize()
+            log(f"composed {copies} page copies (untimed, as at prefill)")
+
+        def step(i):
+            s = sets[i % copies]
+            if host_mode == "zerocopy":
+                c2kv.c2kv_compose_attend(plan, s["host"], s["q"], s["k_suf"], s["v_suf"],
+                                         s["out"], s["lse"])
+            elif host_mode == "load":
+                c2kv.c2kv_load(plan, s["host"], s["pool"])
+                c2kv.c2kv_compose_attend(plan, s["pool"], s["q"], s["k_suf"], s["v_suf"],
+                                         s["out"], s["lse"])
+            elif decode:
+                c2kv.c2kv_attend(plan, s["kp"], s["vp"], s["q"], s["k_suf"], s["v_suf"],
+                                 s["out"], s["lse"])
+            elif long_suffix:
+                c2kv.c2kv_compose(plan, s["pool"], kp, vp)
+                c2kv.c2kv_attend(plan, kp, vp, s["q"], s["k_suf"], s["v_suf"], s["out"],
+                                 s["lse"])
+            else:
+                c2kv.c2kv_compose_attend(plan, s["pool"], s["q"], s["k_suf"], s["v_suf"],
+                                         s["out"], s["lse"])
+
+    ms_per_step, eager_ms, kern, graph_used = time_steps(step, copies, args, c2kv, torch,
+                                                         steps=steps, warmup=warmup,
+                                                         launches_per_step=layers)
+    for s in sets:
+        assert torch.isfinite(s["out"]).all().item(), "non-finite output"
+    ms_per_layer = ms_per_step / layers
+    value = work["tokens"] / (ms_per_layer * 1e-3)
+
+    dom = "attn_paged" if paged else "attn_pool"
+    dom_s = kern[dom]["avg_us"] * 1e-6
+    mfma_bound = idx in (3, 5)
+    if mfma_bound:
+        peak = PEAK_FP32_TFLOPS if w.act_dtype == "f32" else PEAK_BF16_TFLOPS
+        achieved = work["flops"] / dom_s / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                "frac": achieved / peak}
+        dom_bytes = paged_attend_bytes(w, composed) if long_suffix else work["bytes"]
+    else:
+        dom_bytes = paged_attend_bytes(w, composed) if decode else work["bytes"]
+        achieved = dom_bytes / dom_s / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM_GBS}
+    roof["traffic"] = load_traffic(name, dom, dom_bytes)
+    roof["kernel"] = dom
+    roof["kernel_avg_us"] = kern[dom]["avg_us"]
+    roof["algorithmic_bytes"] = dom_bytes
+    roof["algorithmic_flops"] = work["flops"]
+    compose_roof = None
+    if "compose" in kern:
+        # the gather / dequant / re-rotation / page write step on its own: kept rows read
+        # in the storage dtype (and their scales), composed rows written in the
+        # activation dtype
+        b_pool = {"f32": 4, "bf16": 2, "i8": 1}[w.pool_dtype]
+        b_act = {"f32": 4, "bf16": 2}[w.act_dtype]
+        n_tok = int(composed.sum())
+        c_bytes = n_tok * w.n_kv_heads * (2 * w.head_dim * (b_pool + b_act)
+                                          + (8 if w.pool_dtype == "i8" else 0))
+        c_s = kern["compose"]["avg_us"] * 1e-6
+        compose_roof = {"bound": "hbm", "achieved": c_bytes / c_s / 1e9, "peak": PEAK_HBM_GBS,
+                        "unit": "GB/s", "frac": c_bytes / c_s / 1e9 / PEAK_HBM_GBS,
+                        "traffic": load_traffic(name, "compose", c_bytes),
+                        "kernel": "compose", "kernel_avg_us": kern["compose"]["avg_us"],
+                        "algorithmic_bytes": c_bytes}
+
+    result = {
+        "value": value,
+        "unit": "tokens/s/layer",
+        "ms_per_step": ms_per_step,
+        "dtype": "f32" if w.act_dtype == "f32" else "bf16",
+        "config": {"workload": name, "n_q_heads": w.n_q_heads,
+                   "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                   "pool_dtype": w.pool_dtype, "batch": w.batch, "suffix_len": w.suffix_len,
+                   "composed_tokens": work["tokens"], "layers": layers,
+                   "path": ("attend over composed pages" if decode else
+                            "compose+attend" if long_suffix else "compose_attend"),
+                   "plan": {**{k: plan.info[k] for k in ("rows_per_block", "n_work_items",
+                                                         "n_merge_groups", "max_splits")},
+                            "merge_mode": args.merge_mode},
+                   "input_copies": copies, "graph": graph_used},
+        "roofline": roof,
+        **({"compose_roofline": compose_roof} if compose_roof else {}),
+        "kernels_us": kern,
+        "eager_ms_per_step": eager_ms,
+    }
+    if layers > 1:
+        result["ms_per_layer"] = ms_per_layer
+    if host_mode:
+        link = hosts[0].nbytes                  # every stored row of the compressed chunks
+        result["host_link"] = {"bytes": link, "achieved": link / (ms_per_step * 1e-3) / 1e9,
+                               "peak": PEAK_HOST_LINK_GBS, "unit": "GB/s",
+                               "frac": link / (ms_per_step * 1e-3) / 1e9 / PEAK_HOST_LINK_GBS,
+                               "path": ("kernel reads over the host link" if host_mode == "zerocopy"
+                                        else "copy engines, then the fused kernel")}
+        result["config"]["path"] = result["config"]["path"] + f" (pool in host memory, {host_mode})"
+    if with_cpu:
+        log("timing the float64 oracle on the host (cpu_baseline)")
+        result["cpu_baseline"] = cpu_baseline(w, idx)
+    return result
 
 
 def main():
@@ -327,6 +536,9 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD, choices=sorted(WORKLOADS))
     ap.add_argument("--copies", type=int, default=0, help="input copies to rotate over (0: auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="time only --workload (by default the default workload's run also "
+                         "times the other configurations)")
     ap.add_argument("--no-graph", action="store_true")
     ap.add_argument("--kv-splits", type=int, default=0)
     ap.add_argument("--rows-per-block", type=int, default=0)
@@ -356,171 +568,34 @@ def main():
 
     if args.workload in SIF:
         return run_sif(args, c2kv, synth, torch)
-    idx = WORKLOADS[args.workload]
-    log(f"workload {args.workload}: generating inputs")
-    w = synth.config(idx)
-    host_mode = ("zerocopy" if args.workload in HOST_ZEROCOPY else
-                 "load" if args.workload in HOST_LOAD else None)
-    if host_mode:
-        w = synth.compress_pool(w)
-    plan = c2kv.Plan.for_workload(w, kv_splits=args.kv_splits,
-                                  rows_per_block=args.rows_per_block,
-                                  merge_mode=args.merge_mode).upload()
-    composed, span_end = plan.requests()
-    work = algorithmic_work(w, composed)
-    long_suffix = args.workload in LONG_SUFFIX
-    decode = args.workload in DECODE
-    paged = long_suffix or decode
-    act = torch.float32 if w.act_dtype == "f32" else torch.bfloat16
-
-    # ---- device inputs, replicated so the rotation spans > 2x the Infinity Cache
-    base = dict(k=c2kv.to_device(w.pool_k, w.pool_dtype), v=c2kv.to_device(w.pool_v, w.pool_dtype),
-                ks=None if w.pool_k_scale is None else c2kv.to_device(w.pool_k_scale, "f32"),
-                vs=None if w.pool_v_scale is None else c2kv.to_device(w.pool_v_scale, "f32"),
-                q=c2kv.to_device(w.q, w.act_dtype), k_suf=c2kv.to_device(w.k_suf, w.act_dtype),
-                v_suf=c2kv.to_device(w.v_suf, w.act_dtype))
-    if paged:
-        ksh, vsh = c2kv.page_shapes(plan)
-    if decode:
-        # the step reads the composed pages; each copy gets its own
-        footprint = 2 * math.prod(ksh) * (4 if act == torch.float32 else 2)
-    else:
-        footprint = sum(t.numel() * t.element_size() for t in base.values() if t is not None)
-    copies = args.copies or int(min(64, max(2, math.ceil(2.2 * MALL_BYTES / footprint))))
-    log(f"footprint {footprint / 1e6:.1f} MB per copy, {copies} copies")
-    if host_mode:
-        # host memory is not cached on the device side: two copies, each with its
-        # own device pool (the load destination)
-        copies = args.copies or 2
-        hosts = [c2kv.HostPool(w.pool_k, w.pool_v, w.pool_dtype, w.pool_k_scale,
-                               w.pool_v_scale) for _ in range(copies)]
-        sets = [base] + [{k: (None if t is None else t.clone()) for k, t in base.items()}
-                         for _ in range(copies - 1)]
-        for s, h in zip(sets, hosts):
-            s["host"] = h.desc
-        log(f"host pools: {copies} x {hosts[0].nbytes / 1e6:.1f} MB page-locked")
-    elif decode:
-        sets = [dict(base) for _ in range(copies)]          # pool shared: composed once per copy
-    else:
-        sets = [base] + [{k: (None if t is None else t.clone()) for k, t in base.items()}
-                         for _ in range(copies - 1)]
-    for s in sets:
-        s["pool"] = c2kv.pool_desc(s["k"], s["v"], s["ks"], s["vs"])
-        s["out"] = torch.empty_like(s["q"])
-        s["lse"] = torch.empty((w.batch, w.n_q_heads, w.suffix_len), dtype=torch.float32,
-                               device="cuda")
-    if long_suffix:
-        kp = torch.empty(ksh, dtype=act, device="cuda")
-        vp = torch.empty(vsh, dtype=act, device="cuda")
-    if decode:
-        for s in sets:
-            s["kp"] = torch.empty(ksh, dtype=act, device="cuda")
-            s["vp"] = torch.empty(vsh, dtype=act, device="cuda")
-            c2kv.c2kv_compose(plan, s["pool"], s["kp"], s["vp"])
-        torch.cuda.synchronize()
-        log(f"composed {copies} page copies (untimed, as at prefill)")
-
-    def step(i):
-        s = sets[i % copies]
-        if host_mode == "zerocopy":
-            c2kv.c2kv_compose_attend(plan, s["host"], s["q"], s["k_suf"], s["v_suf"], s["out"],
-                                     s["lse"])
-        elif host_mode == "load":
-            c2kv.c2kv_load(plan, s["host"], s["pool"])
-            c2kv.c2kv_compose_attend(plan, s["pool"], s["q"], s["k_suf"], s["v_suf"], s["out"],
-                                     s["lse"])
-        elif decode:
-            c2kv.c2kv_attend(plan, s["kp"], s["vp"], s["q"], s["k_suf"], s["v_suf"], s["out"],
-                             s["lse"])
-        elif long_suffix:
-            c2kv.c2kv_compose(plan, s["pool"], kp, vp)
-            c2kv.c2kv_attend(plan, kp, vp, s["q"], s["k_suf"], s["v_suf"], s["out"], s["lse"])
-        else:
-            c2kv.c2kv_compose_attend(plan, s["pool"], s["q"], s["k_suf"], s["v_suf"], s["out"],
-                                     s["lse"])
-
-    ms_per_step, eager_ms, kern, graph_used = time_steps(step, copies, args, c2kv, torch)
-    assert torch.isfinite(sets[0]["out"]).all().item(), "non-finite output"
-    K = args.steps
-
-    value = work["tokens"] / (ms_per_step * 1e-3)
-
-    dom = "attn_paged" if paged else "attn_pool"
-    dom_s = kern[dom]["avg_us"] * 1e-6
-    mfma_bound = idx in (3, 5)
-    if mfma_bound:
-        peak = PEAK_FP32_TFLOPS if w.act_dtype == "f32" else PEAK_BF16_TFLOPS
-        achieved = work["flops"] / dom_s / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                "frac": achieved / peak}
-        dom_bytes = paged_attend_bytes(w, composed) if long_suffix else work["bytes"]
-    else:
-        dom_bytes = paged_attend_bytes(w, composed) if decode else work["bytes"]
-        achieved = dom_bytes / dom_s / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": achieved / PEAK_HBM_GBS}
-    roof["traffic"] = load_traffic(args.workload, dom, dom_bytes)
-    roof["kernel"] = dom
-    roof["kernel_avg_us"] = kern[dom]["avg_us"]
-    roof["algorithmic_bytes"] = dom_bytes
-    roof["algorithmic_flops"] = work["flops"]
-    compose_roof = None
-    if "compose" in kern:
-        # the gather / dequant / re-rotation / page write step on its own: kept rows read
-        # in the storage dtype (and their scales), composed rows written in the
-        # activation dtype
-        b_pool = {"f32": 4, "bf16": 2, "i8": 1}[w.pool_dtype]
-        b_act = {"f32": 4, "bf16": 2}[w.act_dtype]
-        n_tok = int(composed.sum())
-        c_bytes = n_tok * w.n_kv_heads * (2 * w.head_dim * (b_pool + b_act)
-                                          + (8 if w.pool_dtype == "i8" else 0))
-        c_s = kern["compose"]["avg_us"] * 1e-6
-        compose_roof = {"bound": "hbm", "achieved": c_bytes / c_s / 1e9, "peak": PEAK_HBM_GBS,
-                        "unit": "GB/s", "frac": c_bytes / c_s / 1e9 / PEAK_HBM_GBS,
-                        "traffic": load_traffic(args.workload, "compose", c_bytes),
-                        "kernel": "compose", "kernel_avg_us": kern["compose"]["avg_us"],
-                        "algorithmic_bytes": c_bytes}
-
+    r = run_workload(args.workload, args, c2kv, torch, args.steps, args.warmup,
+                     with_cpu=not args.no_cpu_baseline)
     result = {
         "metric": METRIC,
-        "value": value,
-        "unit": "tokens/s/layer",
+        "value": r.pop("value"),
+        "unit": r.pop("unit"),
         "n_gpus": 1,
-        "steps": K,
+        "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": r.pop("ms_per_step"),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if w.act_dtype == "f32" else "bf16",
+        "dtype": r.pop("dtype"),
         "data": "synthetic",
-        "config": {"workload": args.workload, "n_q_heads": w.n_q_heads,
-                   "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
-                   "pool_dtype": w.pool_dtype, "batch": w.batch, "suffix_len": w.suffix_len,
-                   "composed_tokens": work["tokens"],
-                   "path": ("attend over composed pages" if decode else
-                            "compose+attend" if long_suffix else "compose_attend"),
-                   "plan": {**{k: plan.info[k] for k in ("rows_per_block", "n_work_items",
-                                                         "n_merge_groups", "max_splits")},
-                            "merge_mode": args.merge_mode},
-                   "input_copies": copies, "graph": graph_used},
-        "roofline": roof,
-        **({"compose_roofline": compose_roof} if compose_roof else {}),
-        "kernels_us": kern,
-        "eager_ms_per_step": eager_ms,
+        **r,
         "source_sha": kernel_source_sha(),
     }
-    if host_mode:
-        link = hosts[0].nbytes                  # every stored row of the compressed chunks
-        result["host_link"] = {"bytes": link, "achieved": link / (ms_per_step * 1e-3) / 1e9,
-                               "peak": PEAK_HOST_LINK_GBS, "unit": "GB/s",
-                               "frac": link / (ms_per_step * 1e-3) / 1e9 / PEAK_HOST_LINK_GBS,
-                               "path": ("kernel reads over the host link" if host_mode == "zerocopy"
-                                        else "copy engines, then the fused kernel")}
-        result["config"]["path"] = result["config"]["path"] + f" (pool in host memory, {host_mode})"
-    if not args.no_cpu_baseline:
-        log("timing the float64 oracle on the host (cpu_baseline)")
-        result["cpu_baseline"] = cpu_baseline(w, idx)
+    if args.workload == DEFAULT_WORKLOAD and not args.no_configs:
+        # the other configurations, in the same run: their per-layer figures and the
+        # dominant kernel's roofline (inputs freed between them)
+        cfgs = {}
+        for name in SECONDARY:
+            torch.cuda.empty_cache()
+            cfgs[name] = run_workload(name, args, c2kv, torch, SECONDARY_STEPS,
+                                      SECONDARY_WARMUP, with_cpu=False)
+            cfgs[name]["steps"], cfgs[name]["warmup"] = SECONDARY_STEPS, SECONDARY_WARMUP
+        result["configs"] = cfgs
     print(json.dumps(result), flush=True)
 
 

@@ -297,6 +297,45 @@ def build(sp: Spec, layer: int = 0, seed: Optional[int] = None) -> Workload:
         suffix_len=S, q=q, k_suf=k_suf, v_suf=v_suf, keys_pre_rope=sp.keys_pre_rope)
 
 
+def int8_layer_device(sp: Spec, layer: int, seed: int, device: str = "cuda") -> dict:
+    """One layer of an int8-storage workload drawn straight on the device, for
+    timing many layers without generating them on the host: pool K/V as N(0,1)
+    rounded to bf16, then quantised per (row, head) as `quantize_int8` does
+    (scale = max|x| / 127 in float32, codes rint(x / scale) with the division in
+    float64, clipped to +-127); q, k_suf, v_suf as N(0,1) in bf16.  Seeded by
+    (seed, layer) through torch's device generator, so the values differ from
+    `build`'s numpy draws of the same layer while following the same recipe.
+    The layout (rows, kept sets) is `build(sp, seed=seed)`'s: rows are indexed
+    the same way.  Returns torch tensors k, v (int8), k_scale, v_scale (float32),
+    q, k_suf, v_suf (bf16)."""
+    import torch
+    if sp.pool_dtype != "i8":
+        raise ValueError("int8_layer_device draws int8-storage workloads only")
+    states = np.random.SeedSequence([seed, 7919, layer, 2]).generate_state(5)
+    gens = [torch.Generator(device=device) for _ in states]
+    for g, st in zip(gens, states):
+        g.manual_seed(int(st))
+    rows = sp.prefix_len + sp.n_pool_chunks * sp.chunk_len
+    H, D, B, S = sp.n_kv_heads, sp.head_dim, sp.batch, sp.suffix_len
+
+    def normal_bf16(g, shape):
+        return torch.randn(shape, generator=g, device=device, dtype=torch.float32).to(torch.bfloat16)
+
+    def quant(xb):
+        x = xb.float()
+        scale = x.abs().amax(dim=-1) / 127.0
+        scale = torch.where(scale == 0, torch.ones_like(scale), scale)
+        q = torch.round(x.double() / scale.double()[..., None]).clamp_(-127, 127).to(torch.int8)
+        return q.contiguous(), scale.contiguous()
+
+    k, k_scale = quant(normal_bf16(gens[0], (rows, H, D)))
+    v, v_scale = quant(normal_bf16(gens[1], (rows, H, D)))
+    return dict(k=k, v=v, k_scale=k_scale, v_scale=v_scale,
+                q=normal_bf16(gens[2], (B, S, sp.n_q_heads, D)),
+                k_suf=normal_bf16(gens[3], (B, S, H, D)),
+                v_suf=normal_bf16(gens[4], (B, S, H, D)))
+
+
 @dataclasses.dataclass
 class SifWorkload:
     """Inputs of extraction-time SIF attention: `batch` sequences of n original

@@ -75,3 +75,23 @@ def test_workload_names_match_their_recipes():
             kept = sp.chunk_len if sp.keep == ("all",) else sp.keep[1]
             assert sp.keep[0] in ("all", "count") and kept * r == sp.chunk_len, name
     assert bench.DEFAULT_WORKLOAD in bench.WORKLOADS
+
+
+def test_default_is_the_largest_config_and_the_rest_ride_along():
+    """The headline is the largest single-GPU workload (most flops per layer); the
+    other four configurations are timed in the same run."""
+    flops = {}
+    for name in [bench.DEFAULT_WORKLOAD] + bench.SECONDARY:
+        sp = synth.spec(bench.WORKLOADS[name])
+        kept = sp.keep[1] if sp.keep[0] == "count" else sp.chunk_len * sp.keep[2]
+        n_tok = sp.batch * (sp.prefix_len + sp.chunks_per_req * kept)
+        flops[name] = 4 * sp.n_q_heads * sp.head_dim * n_tok * sp.suffix_len
+    assert max(flops, key=flops.get) == bench.DEFAULT_WORKLOAD == "70b-long-suffix-bf16"
+    assert sorted(bench.WORKLOADS[n] for n in bench.SECONDARY) == [1, 2, 3, 4]
+    assert synth.spec(bench.WORKLOADS["int8-32layer"]).layers == 32
+
+
+def test_cpu_baseline_reports_host_cores():
+    cores, blas = bench.host_threads()
+    assert cores == len(os.sched_getaffinity(0)) and cores >= 1
+    assert blas is None or blas >= 1
