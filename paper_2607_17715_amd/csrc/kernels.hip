@@ -235,6 +235,8 @@ __device__ inline uint4 keep_first(uint4 v, int n_keep) {
 struct AttnParams {
   int Hq, Hkv, G, S, PS, max_pages, RB, n_seg, merge_in_kernel;
   int sif_n, sif_block, sif_sink;  // SIF mask over the suffix when sif_n > 0
+  int tpp;                      // key tiles per page (PS / KT)
+  unsigned tpp_magic;           // floor(2^32 / tpp) + 1 (tpp > 1)
   float qscale;                 // softmax scale * log2(e)
   const int* req_slot0;
   const int2* slot_info;        // (pool row, segment) per composed slot
@@ -507,8 +509,12 @@ struct TileLoader {
   // touch no memory, but still count, so a loop issues the same loads each turn.
   __device__ __forceinline__ void paged_fetch(int k0, uint32_t (&K)[Sh::RKW],
                                               uint32_t (&V)[Sh::RVW], bool real = true) {
-    const size_t ph = size_t(page0 + k0 / a.PS) * a.Hkv + g;
-    const int off = k0 % a.PS;
+    // page of the tile: tile / tiles-per-page as a multiply-high by a reciprocal
+    // computed on the host (exact for the tile counts the plan admits)
+    const unsigned tile = unsigned(k0) / KT;
+    const unsigned prel = a.tpp == 1 ? tile : __umulhi(tile, a.tpp_magic);
+    const size_t ph = size_t(page0 + int(prel)) * a.Hkv + g;
+    const int off = int(tile - prel * unsigned(a.tpp)) * KT;
     const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<T*>(static_cast<const T*>(a.k) + (ph * a.PS + off) * D), 0,
         real ? KT * D * int(sizeof(T)) : 0, kBufferFlags);
@@ -544,7 +550,9 @@ struct TileLoader {
       const int u = tid + i * NT;
       const int d = u / (KT / EPV), vec = u % (KT / EPV);
       uint4 val = make_uint4(V[4 * i], V[4 * i + 1], V[4 * i + 2], V[4 * i + 3]);
-      if (nvalid < KT && vec * EPV + EPV > nvalid) val = keep_first<T>(val, nvalid - vec * EPV);
+      if (nvalid < KT) {                    // a partial tile (uniform): zero past its end
+        if (vec * EPV + EPV > nvalid) val = keep_first<T>(val, nvalid - vec * EPV);
+      }
       uint2* dst = reinterpret_cast<uint2*>(sV + d * L::LDV + vec * EPV);   // 8-byte aligned rows
       dst[0] = make_uint2(val.x, val.y);
       dst[1] = make_uint2(val.z, val.w);
@@ -900,12 +908,11 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
       Op kf[AH];
 #pragma unroll
       for (int f = 0; f < AH; ++f) kf[f] = frag(f);
-#pragma unroll
-      for (int j = 0; j < NKB; ++j) s[j] = bias;
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int f = 0; f < NF; ++f) {
-        s[f / NQC] = M::run(kf[f % AH], qop[f % NQC], s[f / NQC]);
+        // the first product of each chain takes the bias as its accumulator input
+        s[f / NQC] = M::run(kf[f % AH], qop[f % NQC], f % NQC == 0 ? bias : s[f / NQC]);
         if (f + AH < NF) kf[f % AH] = frag(f + AH);
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -913,9 +920,7 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 #pragma unroll
       for (int j = 0; j < NKB; ++j) {
         const int kb = kh * NKB + j;
-        if constexpr (KPL == 8) {
-          s[j] = bias;
-        } else {
+        if constexpr (KPL == 1) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) s[j][v] = 0.f;
         }
@@ -925,7 +930,8 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
           Op ka;
           if constexpr (KPL == 1) ka = krow[c * KSTEP];
           else ka = *reinterpret_cast<const Op*>(krow + c * KSTEP);
-          s[j] = M::run(ka, qop[c], s[j]);
+          // bf16: the first product takes the bias as its accumulator input
+          s[j] = M::run(ka, qop[c], (KPL == 8 && c == 0) ? bias : s[j]);
         }
       }
     }
@@ -1703,6 +1709,8 @@ hipError_t launch_attention(const Plan& p, void* ws, int src_kind, const void* k
   ap.G = p.group;
   ap.S = p.suffix_len;
   ap.PS = p.page_size;
+  ap.tpp = p.page_size / KT;
+  ap.tpp_magic = ap.tpp > 1 ? unsigned((uint64_t(1) << 32) / uint64_t(ap.tpp)) + 1u : 0u;
   ap.max_pages = p.max_pages;
   ap.RB = p.rows_per_block;
   ap.n_seg = p.n_segments;

@@ -235,6 +235,18 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
     pages += np;
   }
   if (pages > kI32Max) { err = "too many pages"; return C2KV_E_UNSUPPORTED; }
+  // the kernels find a tile's page by multiplying with a 32-bit reciprocal of the
+  // tiles per page, exact while tiles * tiles-per-page stays below 2^32
+  {
+    int64_t max_tiles = 0;
+    for (int b = 0; b < B; ++b)
+      max_tiles = std::max<int64_t>(max_tiles, ceil_div(p.req_slot0[b + 1] - p.req_slot0[b],
+                                                        kKeyTile));
+    if ((max_tiles + 4) * (PS / kKeyTile) >= (int64_t(1) << 32)) {
+      err = fmt("page_size ", PS, " too large for requests of ", max_tiles, " key tiles");
+      return C2KV_E_UNSUPPORTED;
+    }
+  }
   p.n_pages = static_cast<int32_t>(pages);
   // compose tiles carry what their workgroup needs, so that it starts with one
   // scalar load: first slot, keys in the tile, page and offset in the page
