@@ -939,13 +939,31 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 
   // ---- causal / ragged-tail mask, then the new running maximum (base 2);
   // accumulator value v of block kb holds key 32*kb + 8*(v/4) + 4*half + v%4
+  // (a tree of three-way maxima: a chain over the lane's 16 NKB scores would
+  // leave every step waiting for the one before)
   auto max_of = [](const f32x16 (&s)[NKB]) {
-    float mt = kNegInf;
+    constexpr int N = 16 * NKB;
+    float x[N];
 #pragma unroll
     for (int j = 0; j < NKB; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) mt = fmaxf(mt, s[j][v]);
-    return mt;
+      for (int v = 0; v < 16; ++v) x[16 * j + v] = s[j][v];
+    int n = N;
+#pragma unroll
+    for (int lvl = 0; lvl < 4; ++lvl) {
+      if (n == 1) break;
+      int m = 0;
+#pragma unroll
+      for (int i = 0; i < N; i += 3) {
+        if (i >= n) break;
+        float r = x[i];
+        if (i + 1 < n) r = fmaxf(r, x[i + 1]);
+        if (i + 2 < n) r = fmaxf(r, x[i + 2]);
+        x[m++] = r;
+      }
+      n = m;
+    }
+    return n == 1 ? x[0] : fmaxf(x[0], x[1]);
   };
   auto mask_max = [&](int tile, f32x16 (&s)[NKB]) {
     const bool suffix = tile >= nct;
@@ -1037,6 +1055,9 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   auto exp_pack = [&](f32x16 (&s)[NKB], float m_ref, Op (&pb)[NPW]) {
     float psum = 0.f;
     if constexpr (KPL == 8) {
+      // four independent partial sums, so that the dot products do not wait for
+      // each other
+      float ps[4] = {0.f, 0.f, 0.f, 0.f};
       typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
       const bf16x2 ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
 #pragma unroll
@@ -1049,9 +1070,10 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
           const bf16x2 pp = {static_cast<__bf16>(p0), static_cast<__bf16>(p1)};
           pb[cc][e] = pp[0];
           pb[cc][e + 1] = pp[1];
-          psum = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, psum, false);
+          ps[e / 2] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, ps[e / 2], false);
         }
       }
+      psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
     }
     return psum;
   };
