@@ -29,6 +29,8 @@ namespace c2kv {
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int KT = kKeyTile;
 constexpr float kNegInf = -__builtin_huge_valf();
@@ -87,10 +89,11 @@ __device__ inline void store8(float* p, const float (&x)[8]) {
   *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
   *reinterpret_cast<float4*>(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
 }
+// (a, b) -> bf16 pair, a in the low half: one paired round-to-nearest-even
+// conversion (two scalar conversions would each need a shift or merge after)
 __device__ inline uint32_t pack_bf16(float a, float b) {
-  const uint32_t lo = __builtin_bit_cast(uint16_t, static_cast<__bf16>(a));
-  const uint32_t hi = __builtin_bit_cast(uint16_t, static_cast<__bf16>(b));
-  return lo | (hi << 16);
+  const f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 __device__ inline void store8(__bf16* p, const float (&x)[8]) {
   uint4 u;
@@ -663,11 +666,6 @@ struct TileLoader {
         if (!Sh::KU_ALL && u >= Sh::KU_TOT) continue;
         const int kk = u / KUPK, c = u % KUPK;
         T* dst = sK + kk * L::LDK + 8 * c;
-        if (nvalid < KT && !k_ok[i]) {        // only a partial tile has such keys
-          store8_zero(dst);
-          store8_zero(dst + HALF);
-          continue;
-        }
         float x[8], y[8];
         if (from_pool) {
           if constexpr (!kPaged) {
@@ -685,6 +683,12 @@ struct TileLoader {
           raw_to_f8<T>(w + Sh::WA, y);
         }
         rotate8(x, y, ck[i], sk[i]);
+        if (nvalid < KT) {                    // only a partial tile (uniform) has keys past
+          if (!k_ok[i]) {                     // its end: written as zeros
+#pragma unroll
+            for (int e = 0; e < 8; ++e) { x[e] = 0.f; y[e] = 0.f; }
+          }
+        }
         store8(dst, x);
         store8(dst + HALF, y);
       }
@@ -723,10 +727,16 @@ struct TileLoader {
           raw_to_f8<T>(w, x0);
           raw_to_f8<T>(w + Sh::WA, x1);
         }
+        if (nvalid < KT) {                    // a partial tile (uniform): zero past its end
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            x0[e] = v_ok[0] ? x0[e] : 0.f;
+            x1[e] = v_ok[1] ? x1[e] : 0.f;
+          }
+        }
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float a0 = v_ok[0] ? x0[e] : 0.f;
-          const float a1 = v_ok[1] ? x1[e] : 0.f;
+          const float a0 = x0[e], a1 = x1[e];
           T* dst = sV + (8 * c + e) * L::LDV + kp2;
           if constexpr (sizeof(T) == 2) {
             *reinterpret_cast<uint32_t*>(dst) = pack_bf16(a0, a1);
@@ -1058,7 +1068,6 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
       // four independent partial sums, so that the dot products do not wait for
       // each other
       float ps[4] = {0.f, 0.f, 0.f, 0.f};
-      typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
       const bf16x2 ones = {static_cast<__bf16>(1.f), static_cast<__bf16>(1.f)};
 #pragma unroll
       for (int cc = 0; cc < NPW; ++cc) {
@@ -1067,7 +1076,8 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         for (int e = 0; e < KPL; e += 2) {
           const float p0 = __builtin_amdgcn_exp2f(s[j][v0 + e] - m_ref);
           const float p1 = __builtin_amdgcn_exp2f(s[j][v0 + e + 1] - m_ref);
-          const bf16x2 pp = {static_cast<__bf16>(p0), static_cast<__bf16>(p1)};
+          const f32x2 p01 = {p0, p1};
+          const bf16x2 pp = __builtin_convertvector(p01, bf16x2);   // one paired conversion
           pb[cc][e] = pp[0];
           pb[cc][e + 1] = pp[1];
           ps[e / 2] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, ps[e / 2], false);
