@@ -1365,15 +1365,19 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 // ----------------------------------------------------------------------------
 
 // Rows of one merge group, RPW per workgroup, TPR threads per row with EPT
-// output elements each.  Two dependent memory steps: the split LSEs (reduced
-// across the row's threads into per-split weights in LDS), then the partial
-// rows of up to 16 splits at a time, all loads of a batch in flight together.
+// output elements each.  The split LSEs and the partial rows of the first NB
+// splits are loaded together (their addresses do not depend on each other),
+// so that up to NB splits take one memory round trip; the LSEs are reduced
+// across the row's threads into per-split weights in LDS.  Later batches of NB
+// splits each take one more.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
   constexpr int EPT = 4;
   constexpr int TPR = D / EPT;                 // threads per row
   constexpr int RPW = 256 / TPR;               // rows per workgroup
   constexpr int NPS = kMaxSplits / TPR;        // split LSEs per thread
+  constexpr int NB = 16;                       // splits per batch of partial-row loads
+  constexpr int WPE = EPT * sizeof(T) / 4;     // 32-bit words of a thread's elements
   __shared__ float s_w[kMaxSplits][RPW];
   const MergeGroup mg = a.groups[blockIdx.x];
   const int rlo = blockIdx.y * RPW;
@@ -1390,23 +1394,19 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
   float li[NPS];
 #pragma unroll
   for (int k = 0; k < NPS; ++k) li[k] = pl[size_t(min(sub + k * TPR, last)) * a.RB];
-  // the first 16 splits' partial rows load together with the LSEs (their
-  // addresses do not depend on them): one memory round trip instead of two
   const T* po = static_cast<const T*>(a.part_o) + (size_t(mg.part0) * a.RB + rloc) * D + sub * EPT;
-  float v[16][EPT];
+  uint32_t w[NB][WPE];                         // raw partial elements, decoded at use
   auto load_batch = [&](int i0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const T* src = po + size_t(min(i0 + k, last)) * a.RB * D;
-      if constexpr (sizeof(T) == 4) {
-        const float4 x = *reinterpret_cast<const float4*>(src);
-        v[k][0] = x.x; v[k][1] = x.y; v[k][2] = x.z; v[k][3] = x.w;
+    for (int k = 0; k < NB; ++k) {
+      const uint32_t* src =
+          reinterpret_cast<const uint32_t*>(po + size_t(min(i0 + k, last)) * a.RB * D);
+      if constexpr (WPE == 4) {
+        const uint4 x = *reinterpret_cast<const uint4*>(src);
+        w[k][0] = x.x; w[k][1] = x.y; w[k][2] = x.z; w[k][3] = x.w;
       } else {
-        const uint2 u = *reinterpret_cast<const uint2*>(src);
-        v[k][0] = __uint_as_float(u.x << 16);
-        v[k][1] = __uint_as_float(u.x & 0xffff0000u);
-        v[k][2] = __uint_as_float(u.y << 16);
-        v[k][3] = __uint_as_float(u.y & 0xffff0000u);
+        const uint2 x = *reinterpret_cast<const uint2*>(src);
+        w[k][0] = x.x; w[k][1] = x.y;
       }
     }
   };
@@ -1432,14 +1432,24 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
   __syncthreads();
 
   float acc[EPT] = {};
-  for (int i0 = 0; i0 < mg.nsplit; i0 += 16) {
+  for (int i0 = 0; i0 < mg.nsplit; i0 += NB) {
     if (i0 > 0) load_batch(i0);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
+    for (int k = 0; k < NB; ++k) {
       const int i = i0 + k;
-      const float w = s_w[min(i, last)][rl] * (i <= last ? 1.f : 0.f);
+      const float wt = s_w[min(i, last)][rl] * (i <= last ? 1.f : 0.f);
+      float v[EPT];
+      if constexpr (WPE == 4) {
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) acc[e] += w * v[k][e];
+        for (int e = 0; e < EPT; ++e) v[e] = __uint_as_float(w[k][e]);
+      } else {
+        v[0] = __uint_as_float(w[k][0] << 16);
+        v[1] = __uint_as_float(w[k][0] & 0xffff0000u);
+        v[2] = __uint_as_float(w[k][1] << 16);
+        v[3] = __uint_as_float(w[k][1] & 0xffff0000u);
+      }
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) acc[e] += wt * v[e];
     }
   }
   if (!ok) return;
@@ -1460,15 +1470,17 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
 
 // One row per workgroup, the splits spread over SPL split lanes of TPR threads
 // (row blocks with few rows and many splits: decode, short suffixes).  Each
-// thread reads its splits' LSEs and partial elements in one batch of loads; the
-// maximum, the sum of weights and the weighted rows are reduced across lanes
-// through LDS.  SPB splits per lane per batch.
+// thread loads its first SPB splits' LSEs and partial elements together, so that
+// up to SPL * SPB splits take one memory round trip; the maximum, the sum of
+// weights and the weighted rows are reduced across lanes through LDS.  Later
+// batches of SPB splits per lane each take one more.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void merge_split_kernel(MergeParams a) {
   constexpr int EPT = 4;
   constexpr int TPR = D / EPT;                 // threads per row
   constexpr int SPL = 256 / TPR;               // split lanes
   constexpr int SPB = 8;                       // splits per lane per batch
+  constexpr int WPE = EPT * sizeof(T) / 4;     // 32-bit words of a thread's elements
   __shared__ float s_red[256];
   __shared__ float s_acc[SPL][D];
   const MergeGroup mg = a.groups[blockIdx.x];
@@ -1479,14 +1491,38 @@ __global__ __launch_bounds__(256) void merge_split_kernel(MergeParams a) {
   const float* pl = a.part_lse + size_t(mg.part0) * a.RB + rloc;
   const T* po = static_cast<const T*>(a.part_o) + (size_t(mg.part0) * a.RB + rloc) * D + sub * EPT;
 
-  // maximum over all split LSEs: every thread reads the splits of its lane
+  // a batch: splits i0 + k * SPL, k < SPB, from indices clamped to the last
+  // split (unconditional loads; what lies past it gets weight zero)
+  float l[SPB];
+  uint32_t w[SPB][WPE];
+  auto load_batch = [&](int i0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k = 0; k < SPB; ++k) {
+      const int i = min(i0 + k * SPL, last);
+      l[k] = pl[size_t(i) * a.RB];
+      const uint32_t* src = reinterpret_cast<const uint32_t*>(po + size_t(i) * a.RB * D);
+      if constexpr (WPE == 4) {
+        const uint4 x = *reinterpret_cast<const uint4*>(src);
+        w[k][0] = x.x; w[k][1] = x.y; w[k][2] = x.z; w[k][3] = x.w;
+      } else {
+        const uint2 x = *reinterpret_cast<const uint2*>(src);
+        w[k][0] = x.x; w[k][1] = x.y;
+      }
+    }
+  };
+  load_batch(sl);
+
+  // maximum over all split LSEs: the first batch's from registers, any later
+  // batch's (LSEs only) read now
   float mx = kNegInf;
-  for (int i0 = sl; i0 <= last; i0 += SPL * SPB) {
-    float l[SPB];
 #pragma unroll
-    for (int k = 0; k < SPB; ++k) l[k] = pl[size_t(min(i0 + k * SPL, last)) * a.RB];
+  for (int k = 0; k < SPB; ++k) mx = fmaxf(mx, sl + k * SPL <= last ? l[k] : kNegInf);
+  for (int i0 = sl + SPL * SPB; i0 <= last; i0 += SPL * SPB) {
+    float lk[SPB];
 #pragma unroll
-    for (int k = 0; k < SPB; ++k) mx = fmaxf(mx, i0 + k * SPL <= last ? l[k] : kNegInf);
+    for (int k = 0; k < SPB; ++k) lk[k] = pl[size_t(min(i0 + k * SPL, last)) * a.RB];
+#pragma unroll
+    for (int k = 0; k < SPB; ++k) mx = fmaxf(mx, i0 + k * SPL <= last ? lk[k] : kNegInf);
   }
   s_red[tid] = mx;
   __syncthreads();
@@ -1498,29 +1534,23 @@ __global__ __launch_bounds__(256) void merge_split_kernel(MergeParams a) {
   // weighted partial rows of this lane's splits
   float z = 0.f, acc[EPT] = {};
   for (int i0 = sl; i0 <= last; i0 += SPL * SPB) {
-    float l[SPB], v[SPB][EPT];
+    if (i0 != sl) load_batch(i0);
 #pragma unroll
     for (int k = 0; k < SPB; ++k) {
-      const int i = min(i0 + k * SPL, last);
-      l[k] = pl[size_t(i) * a.RB];
-      const T* src = po + size_t(i) * a.RB * D;
-      if constexpr (sizeof(T) == 4) {
-        const float4 x = *reinterpret_cast<const float4*>(src);
-        v[k][0] = x.x; v[k][1] = x.y; v[k][2] = x.z; v[k][3] = x.w;
+      const float wt = (i0 + k * SPL <= last && l[k] != kNegInf) ? __expf(l[k] - mx) : 0.f;
+      float v[EPT];
+      if constexpr (WPE == 4) {
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) v[e] = __uint_as_float(w[k][e]);
       } else {
-        const uint2 u = *reinterpret_cast<const uint2*>(src);
-        v[k][0] = __uint_as_float(u.x << 16);
-        v[k][1] = __uint_as_float(u.x & 0xffff0000u);
-        v[k][2] = __uint_as_float(u.y << 16);
-        v[k][3] = __uint_as_float(u.y & 0xffff0000u);
+        v[0] = __uint_as_float(w[k][0] << 16);
+        v[1] = __uint_as_float(w[k][0] & 0xffff0000u);
+        v[2] = __uint_as_float(w[k][1] << 16);
+        v[3] = __uint_as_float(w[k][1] & 0xffff0000u);
       }
-    }
+      z += wt;
 #pragma unroll
-    for (int k = 0; k < SPB; ++k) {
-      const float w = (i0 + k * SPL <= last && l[k] != kNegInf) ? __expf(l[k] - mx) : 0.f;
-      z += w;
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) acc[e] += w * v[k][e];
+      for (int e = 0; e < EPT; ++e) acc[e] += wt * v[e];
     }
   }
   // lane sums: z from the sub == 0 thread of each lane, the rows element-wise
