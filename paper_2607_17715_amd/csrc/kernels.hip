@@ -433,10 +433,7 @@ struct TileLoader {
   int nv[2];                                // pool rows of its values (only the row: a
                                             // loaded word left unused would be reused
                                             // while its load is in flight)
-  bool nk_ok[Sh::NKU], nv_ok[2];            // which of them are inside the tile
   uint32_t kofs[Sh::NPK], vofs[Sh::NPV];    // paged: byte offsets of this thread's vectors
-  bool k_ok[Sh::NKU];
-  bool v_ok[2];
   float k_scale[Sh::NKU], v_scale[2];
 
   __device__ __forceinline__ TileLoader(const AttnParams& a_, int tid_, int b_, int g_, int slot0_,
@@ -449,13 +446,10 @@ struct TileLoader {
 #pragma unroll
     for (int i = 0; i < Sh::NKU; ++i) {
       nk[i] = make_int2(0, -1);
-      nk_ok[i] = false;
       cs_seg[i] = -1;
-      k_ok[i] = false;
       k_scale[i] = 1.f;
     }
     nv[0] = nv[1] = 0;
-    nv_ok[0] = nv_ok[1] = false;
     if constexpr (kPaged) {
       constexpr int EPV = Sh::EPV;
 #pragma unroll
@@ -469,14 +463,15 @@ struct TileLoader {
         vofs[i] = uint32_t((u / (KT / EPV)) * a.PS + (u % (KT / EPV)) * EPV) * sizeof(T);
       }
     }
-    v_ok[0] = v_ok[1] = false;
     v_scale[0] = v_scale[1] = 1.f;
   }
 
   // Every load here and in fetch_data is unconditional, from a clamped index
-  // inside the tile (validity is kept apart): a load whose destination was
-  // first set to a default would make the compiler wait for all loads in
-  // flight, including the row loads of the tile after next.
+  // inside the tile: a load whose destination was first set to a default would
+  // make the compiler wait for all loads in flight, including the row loads of
+  // the tile after next.  Past a partial tile's end the keys and values are
+  // therefore copies of its last row (finite); the mask takes those keys' scores
+  // to -inf, so their probabilities are exactly zero and nothing is zeroed.
   // SUF: the tile is a suffix tile (tile >= nct), known at compile time so
   // that a loop runs one kind of tile and its loads have one set of registers.
   template <bool SUF>
@@ -493,12 +488,10 @@ struct TileLoader {
       for (int i = 0; i < Sh::NKU; ++i) {
         const int u = tid + i * NT;
         const int kk = u / KUPK;
-        nk_ok[i] = u < Sh::KU_TOT && kk < nvalid;
         nk[i] = a.slot_info[slot0 + k0 + min(kk, nvalid - 1)];
       }
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        nv_ok[j] = kp2 + j < nvalid;
         nv[j] = a.slot_info[slot0 + k0 + min(kp2 + j, nvalid - 1)].x;
       }
     }
@@ -583,7 +576,6 @@ struct TileLoader {
         const int u = tid + i * NT;
         const int kk = u / KUPK, c = u % KUPK;
         uint32_t* w = rk + i * 2 * Sh::WA;
-        k_ok[i] = u < Sh::KU_TOT && kk < nvalid;
         if (Sh::KU_ALL || u < Sh::KU_TOT) {   // uniform per wavefront
           const size_t tok = size_t(b) * S + k0 + min(kk, nvalid - 1);
           const size_t row = tok * a.Hkv + g;
@@ -600,7 +592,6 @@ struct TileLoader {
         uint32_t* w = rv + i * 2 * Sh::WA;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          v_ok[j] = u < Sh::VU_TOT && kp2 + j < nvalid;
           if (Sh::VU_ALL || u < Sh::VU_TOT) {
             const size_t row = (size_t(b) * S + k0 + min(kp2 + j, nvalid - 1)) * a.Hkv + g;
             raw_load8<T>(w + j * Sh::WA, vsuf + row * D + 8 * c);
@@ -621,7 +612,6 @@ struct TileLoader {
         uint32_t* w = rv + i * 2 * Sh::WP;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          v_ok[j] = u < Sh::VU_TOT && nv_ok[j];
           if (Sh::VU_ALL || u < Sh::VU_TOT) {
             const size_t row = size_t(nv[j]) * a.Hkv + g;
             raw_load8<PoolT>(w + j * Sh::WP, vpool + row * D + 8 * c);
@@ -634,7 +624,6 @@ struct TileLoader {
         const int u = tid + i * NT;
         const int c = u % KUPK;
         uint32_t* w = rk + i * 2 * Sh::WP;
-        k_ok[i] = nk_ok[i];
         if (Sh::KU_ALL || u < Sh::KU_TOT) {
           const size_t row = size_t(nk[i].x) * a.Hkv + g;
           raw_load8<PoolT>(w, kpool + row * D + 8 * c);
@@ -683,12 +672,6 @@ struct TileLoader {
           raw_to_f8<T>(w + Sh::WA, y);
         }
         rotate8(x, y, ck[i], sk[i]);
-        if (nvalid < KT) {                    // only a partial tile (uniform) has keys past
-          if (!k_ok[i]) {                     // its end: written as zeros
-#pragma unroll
-            for (int e = 0; e < 8; ++e) { x[e] = 0.f; y[e] = 0.f; }
-          }
-        }
         store8(dst, x);
         store8(dst + HALF, y);
       }
@@ -700,7 +683,7 @@ struct TileLoader {
         // bf16 values that need no decode: a transposed word holds element e of
         // the two keys kp2 and kp2 + 1, i.e. one 16-bit half of each row's word
         constexpr bool kRawV = sizeof(T) == 2 && !(from_pool && SRC == SRC_POOL_I8);
-        if (kRawV && nvalid == KT) {
+        if (kRawV) {
           const uint32_t* w0 = rv + i * 2 * (from_pool ? Sh::WP : Sh::WA);
           const uint32_t* w1 = w0 + (from_pool ? Sh::WP : Sh::WA);
 #pragma unroll
@@ -726,13 +709,6 @@ struct TileLoader {
           const uint32_t* w = rv + i * 2 * Sh::WA;
           raw_to_f8<T>(w, x0);
           raw_to_f8<T>(w + Sh::WA, x1);
-        }
-        if (nvalid < KT) {                    // a partial tile (uniform): zero past its end
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            x0[e] = v_ok[0] ? x0[e] : 0.f;
-            x1[e] = v_ok[1] ? x1[e] : 0.f;
-          }
         }
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
