@@ -89,6 +89,21 @@ def test_decode_16k_grid(idx):
     _both_paths(synth.config(idx), synth.spec(idx).name)
 
 
+@pytest.mark.parametrize("head_dim,kv_splits", [(128, 64), (128, 65), (128, 200),
+                                                (64, 128), (64, 129), (64, 256)])
+def test_merge_many_splits(head_dim, kv_splits):
+    """Row blocks of a few rows with many splits are combined one row per
+    workgroup, each lane loading a batch of splits (64 at D = 128, 128 at D = 64)
+    with the LSEs; counts at, just past and well past one batch take the later
+    batches' path.  16384 composed tokens: 256 key tiles per kv-head."""
+    sp = synth.Spec("merge-many", 8, 2, head_dim, 5e5, "bf16", "bf16", 4, 4096, 0, 1, 4,
+                    "natural", ("all",), 2)
+    w = synth.build(sp, seed=23)
+    plan = _both_paths(w, f"merge-many D={head_dim} splits={kv_splits}", kv_splits=kv_splits)
+    assert plan.info["max_splits"] == kv_splits
+    assert plan.info["rows_per_block"] <= 128
+
+
 @pytest.mark.parametrize("suffix_len", [1, 7, 25])
 @pytest.mark.parametrize("opts", [dict(kv_splits=1), dict(kv_splits=2), dict(kv_splits=3),
                                   dict(kv_splits=5), dict(kv_splits=3, page_size=128)])
