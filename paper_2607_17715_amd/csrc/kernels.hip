@@ -289,12 +289,19 @@ struct MergeParams {
 
 template <typename T, int D>
 struct Lds {
-  // keys: rows of D elements padded by 16 bytes (16-byte reads, 4-bank row shift);
-  // transposed values: rows of KT keys padded by 8 bytes, so that 32 consecutive
-  // rows map 8-byte reads onto distinct bank pairs
+  // keys: rows of D elements padded by 16 bytes (16-byte reads, 4-bank row shift).
+  // Transposed values, bf16: rows of KT keys padded by 16 bytes, with the keys of
+  // each group of 16 stored in the order 0-3, 8-11, 4-7, 12-15, so that the 8 keys
+  // one lane feeds to a P*V product (4h..4h+3 and 8+4h..8+4h+3 of a group, h the
+  // lane's half) are one 16-byte read; 16 consecutive rows of such reads fall on
+  // distinct banks.  fp32: rows padded by 8 bytes, natural key order.
   static constexpr int LDK = D + 16 / int(sizeof(T));
-  static constexpr int LDV = KT + 8 / int(sizeof(T));
+  static constexpr int LDV = KT + (sizeof(T) == 2 ? 16 : 8) / int(sizeof(T));
   static constexpr int TILE = KT * LDK + D * LDV;   // elements of one stage
+  // column of key k in a transposed value row (swaps bits 2 and 3 of k for bf16)
+  __device__ static constexpr int vcol(int k) {
+    return sizeof(T) == 2 ? (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1) : k;
+  }
 };
 
 constexpr int imax(int a, int b) { return a > b ? a : b; }
@@ -549,9 +556,11 @@ struct TileLoader {
       if (nvalid < KT) {                    // a partial tile (uniform): zero past its end
         if (vec * EPV + EPV > nvalid) val = keep_first<T>(val, nvalid - vec * EPV);
       }
-      uint2* dst = reinterpret_cast<uint2*>(sV + d * L::LDV + vec * EPV);   // 8-byte aligned rows
-      dst[0] = make_uint2(val.x, val.y);
-      dst[1] = make_uint2(val.z, val.w);
+      // the vector's two 8-byte halves (bf16: keys 8 vec + 0..3 and + 4..7), each to
+      // its column
+      T* row = sV + d * L::LDV;
+      *reinterpret_cast<uint2*>(row + L::vcol(vec * EPV)) = make_uint2(val.x, val.y);
+      *reinterpret_cast<uint2*>(row + L::vcol(vec * EPV + EPV / 2)) = make_uint2(val.z, val.w);
     }
   }
   // cached paged tile `tile` into / out of register set B
@@ -688,7 +697,7 @@ struct TileLoader {
           const uint32_t* w1 = w0 + (from_pool ? Sh::WP : Sh::WA);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            T* dst = sV + (8 * c + e) * L::LDV + kp2;
+            T* dst = sV + (8 * c + e) * L::LDV + L::vcol(kp2);
             *reinterpret_cast<uint32_t*>(dst) =
                 __builtin_amdgcn_perm(w1[e / 2], w0[e / 2], (e & 1) ? 0x07060302u : 0x05040100u);
           }
@@ -713,7 +722,7 @@ struct TileLoader {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float a0 = x0[e], a1 = x1[e];
-          T* dst = sV + (8 * c + e) * L::LDV + kp2;
+          T* dst = sV + (8 * c + e) * L::LDV + L::vcol(kp2);
           if constexpr (sizeof(T) == 2) {
             *reinterpret_cast<uint32_t*>(dst) = pack_bf16(a0, a1);
           } else {
@@ -1064,7 +1073,8 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
     return psum;
   };
   // ---- O^T += V^T P^T; chunk c of the tile covers keys 16*(c%2) + 4*half +
-  // {0..3} and + 8 + {0..3} of block c / 2
+  // {0..3} and + 8 + {0..3} of block c / 2 (bf16: one 16-byte read at column
+  // 16*(c%2) + 8*half of the block's permuted row)
   auto pv = [&](const T* sV, const Op (&pb)[NPW]) {
     if constexpr (KPL == 8 && kPaged) {
       // value fragments in a ring of AH ahead of their MFMAs, as for the keys
@@ -1072,10 +1082,8 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
       auto frag = [&](int f) {
         const int cc = f / NDB, db = f % NDB;
         const int c = kh * NPW + cc;
-        const T* vrow = sV + (db * 32 + qi) * L::LDV + (c / CPB) * 32 + 4 * half + 16 * (c % CPB);
-        const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
-        return __builtin_bit_cast(Op, make_uint4(lo.x, lo.y, hi.x, hi.y));
+        const T* vrow = sV + (db * 32 + qi) * L::LDV + (c / CPB) * 32 + 8 * half + 16 * (c % CPB);
+        return *reinterpret_cast<const Op*>(vrow);
       };
       Op vf[AH];
 #pragma unroll
@@ -1095,11 +1103,8 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
         const int kofs = 16 * (c % CPB);
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const T* vrow = sV + (db * 32 + qi) * L::LDV + kb * 32 + 4 * half + kofs;
-          const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
-          o[db] = M::run(__builtin_bit_cast(Op, make_uint4(lo.x, lo.y, hi.x, hi.y)), pb[cc],
-                         o[db]);
+          const T* vrow = sV + (db * 32 + qi) * L::LDV + kb * 32 + 8 * half + kofs;
+          o[db] = M::run(*reinterpret_cast<const Op*>(vrow), pb[cc], o[db]);
         }
       }
     }
