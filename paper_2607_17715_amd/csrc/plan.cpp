@@ -342,14 +342,16 @@ c2kv_status build_plan(const c2kv_attn_cfg& cfg, const c2kv_compose_desc& d,
     for (const auto& x : gr.ranges) {
       const int32_t len = x.second - x.first;
       int32_t k = o.kv_splits > 0 ? o.kv_splits : ceil_div(len, per_item);
-      // with splits and one workgroup per CU, take as many as one round of
-      // workgroups holds (the longest item keeps its tile count; the CUs the
-      // rounding left idle get work).  Measured: int8 layer -1.2 %; at two
-      // workgroups per CU (decode) it helped compressed contexts and cost the
-      // long uncompressed ones up to 5 %, so those keep the rounded count.
-      if (o.kv_splits == 0 && split && wgs_per_cu == 1)
-        k = std::max<int32_t>(k, std::min<int64_t>(len, target / int64_t(groups.size()) /
-                                                            int64_t(gr.ranges.size())));
+      // With splits, take as many as one round of workgroups holds: the longest
+      // item keeps its tile count and the CUs the rounding left idle get work.
+      // Measured: int8 layer (one workgroup per CU) -1.2 %; at two workgroups
+      // per CU (decode) -7 % where the items then hold at most 4 tiles, and up
+      // to +5 % for the long uncompressed contexts, which keep the rounded count.
+      if (o.kv_splits == 0 && split) {
+        const int32_t fill = static_cast<int32_t>(
+            std::min<int64_t>(len, target / int64_t(groups.size()) / int64_t(gr.ranges.size())));
+        if (fill > k && (wgs_per_cu == 1 || ceil_div(len, fill) <= 4)) k = fill;
+      }
       k = std::max(1, std::min({k, len, kMaxSplits / int32_t(gr.ranges.size())}));
       nsr.push_back(k);
       ns += k;
