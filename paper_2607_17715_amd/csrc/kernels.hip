@@ -1176,9 +1176,11 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
   // but computes nothing
   const bool rows_here = rgrp * 32 < it.nrows;
 
-  // bf16 pages with 128-row blocks (short suffixes, decode: bandwidth-bound) keep
-  // two tiles' loads in flight, in two register sets that alternate
-  constexpr bool kDeep = kPaged && KG == 2 && NT == 512 && sizeof(T) == 2;
+  // bf16 pages with 512-thread workgroups keep two tiles' loads in flight, in two
+  // register sets that alternate: for 128-row blocks (short suffixes, decode:
+  // bandwidth-bound) and for 256-row blocks (long suffixes), where one tile of
+  // compute did not cover the row loads' latency
+  constexpr bool kDeep = kPaged && NT == 512 && sizeof(T) == 2;
 
   // Tiles [ta, tb) of one kind.  Prologue: tile ta (its loads issued already
   // when `fetched`) into stage 0, tile ta + 1 in registers.  The loads of a
