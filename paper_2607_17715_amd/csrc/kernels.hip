@@ -214,19 +214,18 @@ __device__ inline void raw_to_f8(const uint32_t* w, float (&x)[8]) {
   }
 }
 
-// zero the elements [n_keep, 16 / sizeof(T)) of a 16-byte vector
+// zero the elements [n_keep, 16 / sizeof(T)) of a 16-byte vector (a mask per
+// word from selects, no branches: n_keep differs between lanes)
 template <typename T>
 __device__ inline uint4 keep_first(uint4 v, int n_keep) {
   uint32_t w[4] = {v.x, v.y, v.z, v.w};
   constexpr int EPW = 4 / sizeof(T);              // elements per word
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    if constexpr (EPW == 1) {
-      if (i >= n_keep) w[i] = 0u;
-    } else {
-      if (2 * i >= n_keep) w[i] = 0u;
-      else if (2 * i + 1 >= n_keep) w[i] &= 0x0000ffffu;
-    }
+    const int k = n_keep - EPW * i;               // elements of word i to keep
+    uint32_t m = k >= EPW ? 0xffffffffu : 0u;
+    if constexpr (EPW == 2) m = k == 1 ? 0x0000ffffu : m;
+    w[i] &= m;
   }
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
