@@ -1351,14 +1351,16 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 // splits are loaded together (their addresses do not depend on each other),
 // so that up to NB splits take one memory round trip; the LSEs are reduced
 // across the row's threads into per-split weights in LDS.  Later batches of NB
-// splits each take one more.
+// splits each take one more.  Partial rows are loaded only for the group's own
+// splits (a branch uniform over the workgroup): clamped duplicates to fill a
+// batch of 32 cost more than a second round trip.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
   constexpr int EPT = 4;
   constexpr int TPR = D / EPT;                 // threads per row
   constexpr int RPW = 256 / TPR;               // rows per workgroup
   constexpr int NPS = kMaxSplits / TPR;        // split LSEs per thread
-  constexpr int NB = 16;                       // splits per batch of partial-row loads
+  constexpr int NB = 32;                       // splits per batch of partial-row loads
   constexpr int WPE = EPT * sizeof(T) / 4;     // 32-bit words of a thread's elements
   __shared__ float s_w[kMaxSplits][RPW];
   const MergeGroup mg = a.groups[blockIdx.x];
@@ -1369,9 +1371,9 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
   const bool ok = rloc < mg.nrows;
   const float* pl = a.part_lse + size_t(mg.part0) * a.RB + rloc;
 
-  // Loads are unconditional, from indices clamped into the group's partials
-  // (rows of a partial exist up to RB), so that no load waits at a branch join;
-  // what lies past the row count or the split count gets weight zero.
+  // LSE loads are unconditional, from indices clamped into the group's partials
+  // (rows of a partial exist up to RB); what lies past the row count or the
+  // split count gets weight zero.
   const int last = mg.nsplit - 1;
   float li[NPS];
 #pragma unroll
@@ -1381,8 +1383,9 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
   auto load_batch = [&](int i0) __attribute__((always_inline)) {
 #pragma unroll
     for (int k = 0; k < NB; ++k) {
+      if (i0 + k > last) break;                // uniform: this group's splits only
       const uint32_t* src =
-          reinterpret_cast<const uint32_t*>(po + size_t(min(i0 + k, last)) * a.RB * D);
+          reinterpret_cast<const uint32_t*>(po + size_t(i0 + k) * a.RB * D);
       if constexpr (WPE == 4) {
         const uint4 x = *reinterpret_cast<const uint4*>(src);
         w[k][0] = x.x; w[k][1] = x.y; w[k][2] = x.z; w[k][3] = x.w;
@@ -1419,7 +1422,8 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams a) {
 #pragma unroll
     for (int k = 0; k < NB; ++k) {
       const int i = i0 + k;
-      const float wt = s_w[min(i, last)][rl] * (i <= last ? 1.f : 0.f);
+      if (i > last) break;                     // (its partial row was not loaded)
+      const float wt = s_w[i][rl];
       float v[EPT];
       if constexpr (WPE == 4) {
 #pragma unroll
