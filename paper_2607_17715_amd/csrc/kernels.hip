@@ -1320,7 +1320,9 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
 
   // ---- the last split of a row block to finish combines all of its splits
   if (it.merge >= 0 && a.merge_in_kernel) {
-    __threadfence();                       // release this split's partial (agent scope)
+    // release this split's partial at agent scope (every wavefront: its stores are
+    // written back past the L2 of its XCD before the barrier)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
     if (tid == 0) {
       // system scope: the splits of a row block may run on different XCDs, whose
@@ -1332,7 +1334,7 @@ __global__ __launch_bounds__(NT, 2) void attn_kernel(AttnParams a) {
     }
     __syncthreads();
     if (s_last) {
-      __threadfence();                     // acquire the other splits' partials
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // the other splits' partials
       const MergeGroup mg = a.merges[it.merge];
       merge_rows<T, D>(mg, 0, mg.nrows, a.part_o, a.part_lse, a.RB, a.Hq, G, S, a.out, a.lse,
                        tid, NT);
