@@ -104,6 +104,20 @@ def test_merge_many_splits(head_dim, kv_splits):
     assert plan.info["rows_per_block"] <= 128
 
 
+@pytest.mark.parametrize("kv_splits", [17, 32, 33, 65])
+def test_merge_256_row_blocks_batches(kv_splits):
+    """256-row blocks combine their splits in batches of up to 32, loading partial
+    rows for the group's own splits only: one batch past the old 16, exactly one
+    batch, one split past it, and two batches and a split (4160 composed keys and
+    suffix tokens, 65 key tiles per row block)."""
+    sp = synth.Spec("merge-256", 8, 2, 128, 5e5, "bf16", "bf16", 4, 1024, 0, 1, 4,
+                    "natural", ("all",), 64)
+    w = synth.build(sp, seed=29)
+    plan = _both_paths(w, f"merge-256 splits={kv_splits}", kv_splits=kv_splits)
+    assert plan.info["rows_per_block"] == 256
+    assert plan.info["max_splits"] == kv_splits
+
+
 @pytest.mark.parametrize("suffix_len", [1, 7, 25])
 @pytest.mark.parametrize("opts", [dict(kv_splits=1), dict(kv_splits=2), dict(kv_splits=3),
                                   dict(kv_splits=5), dict(kv_splits=3, page_size=128)])
